@@ -1,0 +1,230 @@
+/*
+ * libelis: iterative response-length prediction and ISRTF batch selection
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * ELIS schedules LLM jobs by Iterative Shortest Remaining Time First: at
+ * every scheduling iteration each job that just ran (and each new arrival)
+ * is re-scored by an encoder-based predictor that reads the prompt followed by
+ * the tokens generated so far and outputs the number of tokens the job still
+ * has to produce (Sec. 3.3; Alg. 1); the batcher then forms the batch from
+ * the jobs with the fewest predicted remaining tokens (Sec. 4.1). The
+ * predictor is a BERT-style bidirectional Transformer encoder (BGE, Sec. 3.1)
+ * with a pooled regression head (CLS vector: Sec. 3.2; mean pooling: Sec. 4.2).
+ *
+ * Conventions for every call below:
+ *  - All data pointers are DEVICE pointers owned by the caller, unless a
+ *    comment says "host". The library allocates no device memory, never frees
+ *    caller memory and keeps no state between calls (except the opt-in
+ *    timing facility at the end of this file).
+ *  - Every call validates its scalar arguments on the host, then only
+ *    enqueues kernels on `stream` (a hipStream_t; NULL = the default stream)
+ *    and returns. Nothing synchronises except elis_read_status and
+ *    elis_timing_read.
+ *  - Errors are returned as status codes, never thrown; on an error detected
+ *    on the host nothing is enqueued.
+ *  - bf16 values are passed as their 16-bit patterns (uint16_t).
+ *  - Calls on distinct workspaces may run concurrently; calls that share a
+ *    workspace must be ordered by the caller (same stream).
+ */
+#ifndef ELIS_H
+#define ELIS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------------ status */
+#define ELIS_OK           0
+#define ELIS_EINVAL      -1 /* null pointer, count <= 0, batch_cap < 0, bad config            */
+#define ELIS_ESHAPE      -2 /* max_seqlen > max_pos or < 1, total_tokens < n_seqs, size limit */
+#define ELIS_EWORKSPACE  -3 /* ws_bytes smaller than the matching *_workspace_bytes query      */
+#define ELIS_EHIP        -4 /* a HIP launch or runtime call failed                             */
+#define ELIS_EDEVICE     -5 /* content error found on the device (see elis_read_status)        */
+#define ELIS_EUNSUPPORTED -6 /* a shape this build has no kernel for (see elis_config)          */
+
+/* Device-side content error bits, reported by elis_read_status (ORed). */
+#define ELIS_DEV_BAD_TOKEN   1u  /* a token id outside [0, vocab)                    */
+#define ELIS_DEV_BAD_CU      2u  /* cu_seqlens[0] != 0, not increasing, or != T at n */
+#define ELIS_DEV_LONG_SEQ    4u  /* a sequence longer than max_seqlen               */
+
+/* ------------------------------------------------------------------ model */
+#define ELIS_POOL_CLS  0 /* the first token's final hidden vector (Sec. 3.2)              */
+#define ELIS_POOL_MEAN 1 /* the mean of all of a sequence's final hidden vectors (Sec. 4.2) */
+
+/*
+ * Encoder shape. Supported by this build: d_model % 64 == 0, d_model <= 2048,
+ * d_ff % 64 == 0, d_model / n_heads in {32, 64}, n_layers >= 0, head_hidden
+ * in [0, 4096]. Anything else returns ELIS_EUNSUPPORTED (or ELIS_EINVAL for
+ * non-positive sizes).
+ */
+typedef struct elis_config {
+    int32_t n_layers, d_model, n_heads, d_ff, vocab, max_pos;
+    int32_t pooling;      /* ELIS_POOL_CLS or ELIS_POOL_MEAN                        */
+    int32_t head_hidden;  /* 0: linear d->1; else d->head_hidden->ReLU->1           */
+    float ln_eps;         /* LayerNorm epsilon (biased variance)                   */
+    float out_scale, out_shift; /* prediction = out_shift + out_scale * head output */
+} elis_config;
+
+/* One post-LN encoder layer. Matrices are bf16, row-major [out, in]; the rest fp32. */
+typedef struct elis_layer_weights {
+    const uint16_t *w_qkv; /* [3d, d]: rows 0..d-1 query, d..2d-1 key, 2d..3d-1 value; head h
+                              owns rows h*dh..(h+1)*dh-1 of each block                        */
+    const uint16_t *w_o;   /* [d, d]  */
+    const uint16_t *w_1;   /* [F, d]  */
+    const uint16_t *w_2;   /* [d, F]  */
+    const float *b_qkv, *b_o, *b_1, *b_2;      /* [3d], [d], [F], [d] */
+    const float *ln1_g, *ln1_b, *ln2_g, *ln2_b; /* [d] each            */
+} elis_layer_weights;
+
+typedef struct elis_weights {
+    elis_config cfg;
+    const uint16_t *word;  /* bf16 [vocab, d]   token embedding                 */
+    const uint16_t *pos;   /* bf16 [max_pos, d] learned position embedding      */
+    const float *type0;    /* fp32 [d]          token-type-0 row, added to all  */
+    const float *emb_ln_g, *emb_ln_b;          /* fp32 [d] embedding LayerNorm  */
+    const elis_layer_weights *layers;          /* HOST array of n_layers entries */
+    const float *head_w1;  /* fp32 [head_hidden, d] (unused when head_hidden == 0) */
+    const float *head_b1;  /* fp32 [head_hidden]                                   */
+    const float *head_w2;  /* fp32 [1, head_hidden] or [1, d] for the linear head  */
+    const float *head_b2;  /* fp32 [1]                                             */
+} elis_weights;
+
+/*
+ * Bytes of device workspace elis_predict_remaining needs for these sizes
+ * (0 when the arguments are invalid). The workspace must be 256-byte aligned.
+ */
+size_t elis_predict_workspace_bytes(const elis_config *cfg, int32_t total_tokens,
+                                    int32_t n_seqs, int32_t max_seqlen);
+
+/*
+ * Predicted remaining output tokens of every job of a packed batch
+ * (Sec. 3.3: the target after g generated tokens is total minus g; Alg. 1:
+ * Predictor.init on the prompt, Predictor.iter on prompt followed by the
+ * partial response).
+ *
+ *  token_ids   int32 [total_tokens]: all sequences back to back, no padding.
+ *  cu_seqlens  int32 [n_seqs + 1]: sequence s is token_ids[cu[s] .. cu[s+1]-1];
+ *              cu[0] == 0, cu[n_seqs] == total_tokens, every length >= 1 and
+ *              <= max_seqlen. Positions restart at 0 for every sequence.
+ *  max_seqlen  host int: an upper bound on every length, 1 <= max_seqlen <= max_pos.
+ *  out_pred    fp32 [n_seqs]: out_shift + out_scale * head(pool(H_s)).
+ *  out_hidden  fp32 [total_tokens, d] final hidden states, or NULL.
+ *  workspace   >= elis_predict_workspace_bytes(...) bytes, 256-byte aligned.
+ * Content errors in token_ids / cu_seqlens are detected on the device: the
+ * kernels clamp every index (no out-of-bounds access), the outputs are then
+ * undefined and elis_read_status(workspace) returns ELIS_EDEVICE.
+ */
+int elis_predict_remaining(const elis_weights *w, const int32_t *token_ids,
+                           const int32_t *cu_seqlens, int32_t n_seqs, int32_t total_tokens,
+                           int32_t max_seqlen, float *out_pred, float *out_hidden,
+                           void *workspace, size_t ws_bytes, void *stream);
+
+/* Largest n accepted by elis_isrtf_select in this build. */
+int32_t elis_select_max_n(void);
+
+/* Bytes of device workspace elis_isrtf_select needs for n jobs (0 if n invalid). */
+size_t elis_select_workspace_bytes(int32_t n);
+
+/*
+ * ISRTF batch selection (Sec. 4.1, the Batcher of Alg. 1): the indices of the
+ * min(batch_cap, n) jobs with the fewest predicted remaining tokens, highest
+ * priority first. Ties on the prediction are broken by arrival_seq (earlier
+ * first, the FCFS order of Sec. 6.1), then by index. -0 equals +0; NaN (any
+ * payload) ranks after +inf, all NaNs equal.
+ *
+ *  pred        fp32 [n], arrival_seq int64 [n]
+ *  out_idx     int32 [batch_cap] (only the first min(batch_cap, n) are written)
+ *  out_count   int32 [1] device: set to min(batch_cap, n)
+ * batch_cap == 0 is valid (count 0). 1 <= n <= elis_select_max_n().
+ */
+int elis_isrtf_select(const float *pred, const int64_t *arrival_seq, int32_t n,
+                      int32_t batch_cap, int32_t *out_idx, int32_t *out_count,
+                      void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * Synchronises `stream`, then reads the device error word that the last call
+ * on `workspace` left: ELIS_OK, ELIS_EDEVICE, or ELIS_EHIP. When `bits` is not
+ * NULL (host pointer) the raw ELIS_DEV_* bits are stored there.
+ */
+int elis_read_status(const void *workspace, void *stream, uint32_t *bits);
+
+/* Human-readable name of a status code (static string). */
+const char *elis_status_string(int status);
+
+/* ------------------------------------------------------------------ building blocks
+ * The predictor's kernels, exposed one by one for per-kernel parity tests and
+ * measurement. Same conventions as above.
+ */
+
+/* Epilogues of elis_linear. */
+#define ELIS_EPI_BIAS_BF16      0 /* out bf16 = x W^T + b                        */
+#define ELIS_EPI_BIAS_GELU_BF16 1 /* out bf16 = GELU(x W^T + b), exact erf GELU  */
+#define ELIS_EPI_BIAS_RES_F32   2 /* out fp32 = x W^T + b + residual             */
+
+/*
+ * Dense layer on the matrix cores: out[m, n] = epilogue(sum_k x[m,k] w[n,k] + bias[n]).
+ *  x bf16 [m, k] row-major; w bf16 [n, k] row-major ([out, in]); bias fp32 [n];
+ *  residual fp32 [m, n] (ELIS_EPI_BIAS_RES_F32 only, else ignored).
+ * fp32 accumulation. Requires k % 64 == 0, n % 64 == 0, m >= 1.
+ */
+int elis_linear(const uint16_t *x, const uint16_t *w, const float *bias, const float *residual,
+                int32_t m, int32_t n, int32_t k, int32_t epilogue, void *out, void *stream);
+
+/* Bytes of workspace elis_attention needs (0 if invalid). */
+size_t elis_attention_workspace_bytes(int32_t n_seqs, int32_t total_tokens);
+
+/*
+ * Bidirectional multi-head self-attention within each sequence of a packed
+ * batch: for every head, softmax(q k^T / sqrt(d_head)) v over the tokens of
+ * the same sequence only (an encoder sees its whole input, Sec. 1).
+ *  qkv  bf16 [total_tokens, 3 * n_heads * d_head]: per token, the query, key
+ *       and value blocks, each head-major (head h at h*d_head).
+ *  out  bf16 [total_tokens, n_heads * d_head].
+ * d_head in {32, 64}. cu_seqlens as for elis_predict_remaining; content errors
+ * set bits readable with elis_read_status(workspace).
+ */
+int elis_attention(const uint16_t *qkv, const int32_t *cu_seqlens, int32_t n_seqs,
+                   int32_t total_tokens, int32_t max_seqlen, int32_t n_heads, int32_t d_head,
+                   uint16_t *out, void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * LayerNorm of fp32 rows (biased variance): y = g * (x - mean) / sqrt(var + eps) + b.
+ *  x fp32 [rows, d]; out_f32 fp32 [rows, d] or NULL; out_bf16 bf16 [rows, d] or NULL
+ *  (at least one output). d % 64 == 0, d <= 2048.
+ */
+int elis_layernorm(const float *x, const float *g, const float *b, int32_t rows, int32_t d,
+                   float eps, float *out_f32, uint16_t *out_bf16, void *stream);
+
+/* ------------------------------------------------------------------ timing (opt-in)
+ * When enabled, the library brackets each kernel launch of the classes below
+ * with a pair of HIP events on the launch stream. elis_timing_read
+ * synchronises those events and returns, per class, the number of launches
+ * and the summed kernel time since the last reset. Process-global state; not
+ * thread-safe; meant for benchmarks.
+ */
+#define ELIS_K_SEQMAP    0
+#define ELIS_K_EMBED_LN  1
+#define ELIS_K_GEMM_QKV  2
+#define ELIS_K_ATTENTION 3
+#define ELIS_K_GEMM_O    4
+#define ELIS_K_LAYERNORM 5
+#define ELIS_K_GEMM_FFN1 6
+#define ELIS_K_GEMM_FFN2 7
+#define ELIS_K_POOL_HEAD 8
+#define ELIS_K_SELECT    9
+#define ELIS_K_COUNT     10
+
+int elis_timing_enable(uint32_t class_mask); /* bit c enables class c; 0 disables */
+int elis_timing_reset(void);
+int elis_timing_read(int32_t kernel_class, int32_t *launches, double *total_ms);
+
+/* ABI version of this header: 1. */
+int32_t elis_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ELIS_H */

@@ -1,0 +1,355 @@
+// C ABI of libelis: argument validation, workspace layout and the launch
+// sequence of one predictor forward pass. Every call enqueues on the caller's
+// stream and returns; no device memory is allocated here.
+#include <math.h>
+#include <string.h>
+
+#include <vector>
+
+#include "kernels.h"
+
+using namespace elis;
+
+namespace {
+
+// ------------------------------------------------------------------ timing facility
+struct TimedLaunch {
+    int cls;
+    hipEvent_t a, b;
+};
+uint32_t g_timing_mask = 0;
+std::vector<TimedLaunch> g_pending;
+std::vector<hipEvent_t> g_free_events;
+double g_ms[ELIS_K_COUNT];
+int32_t g_count[ELIS_K_COUNT];
+
+hipEvent_t take_event() {
+    if (!g_free_events.empty()) {
+        hipEvent_t e = g_free_events.back();
+        g_free_events.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Runs one launch; when its class is being timed, brackets it with events.
+template <class F>
+hipError_t timed(int cls, hipStream_t st, F&& launch) {
+    if (!(g_timing_mask & (1u << cls))) return launch();
+    hipEvent_t a = take_event(), b = take_event();
+    if (!a || !b) return hipErrorOutOfMemory;
+    hipError_t e = hipEventRecord(a, st);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(b, st);
+    if (e != hipSuccess) return e;
+    g_pending.push_back({cls, a, b});
+    return hipSuccess;
+}
+
+int status_of(hipError_t e) {
+    if (e == hipSuccess) return ELIS_OK;
+    return e == hipErrorInvalidValue ? ELIS_EINVAL : ELIS_EHIP;
+}
+
+// ------------------------------------------------------------------ validation
+int check_config(const elis_config* c) {
+    if (!c) return ELIS_EINVAL;
+    if (c->n_layers < 0 || c->d_model <= 0 || c->n_heads <= 0 || c->d_ff <= 0 || c->vocab <= 0 ||
+        c->max_pos <= 0 || c->head_hidden < 0)
+        return ELIS_EINVAL;
+    if (c->pooling != ELIS_POOL_CLS && c->pooling != ELIS_POOL_MEAN) return ELIS_EINVAL;
+    if (!(c->ln_eps >= 0.f) || !isfinite(c->out_scale) || !isfinite(c->out_shift)) return ELIS_EINVAL;
+    if (c->d_model % 64 || c->d_model > 2048 || c->d_ff % 64 || c->d_model % c->n_heads) return ELIS_EUNSUPPORTED;
+    const int dh = c->d_model / c->n_heads;
+    if (dh != 32 && dh != 64) return ELIS_EUNSUPPORTED;
+    if (c->head_hidden > 4096) return ELIS_EUNSUPPORTED;
+    return ELIS_OK;
+}
+
+int check_weights(const elis_weights* w) {
+    if (!w) return ELIS_EINVAL;
+    int r = check_config(&w->cfg);
+    if (r != ELIS_OK) return r;
+    if (!w->word || !w->pos || !w->type0 || !w->emb_ln_g || !w->emb_ln_b || !w->head_w2 || !w->head_b2)
+        return ELIS_EINVAL;
+    if (w->cfg.head_hidden > 0 && (!w->head_w1 || !w->head_b1)) return ELIS_EINVAL;
+    if (w->cfg.n_layers > 0 && !w->layers) return ELIS_EINVAL;
+    for (int l = 0; l < w->cfg.n_layers; ++l) {
+        const elis_layer_weights& y = w->layers[l];
+        if (!y.w_qkv || !y.w_o || !y.w_1 || !y.w_2 || !y.b_qkv || !y.b_o || !y.b_1 || !y.b_2 || !y.ln1_g ||
+            !y.ln1_b || !y.ln2_g || !y.ln2_b)
+            return ELIS_EINVAL;
+    }
+    return ELIS_OK;
+}
+
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) == 0; }
+
+// ------------------------------------------------------------------ workspace layout
+struct PredictLayout {
+    size_t status, start, len, tile_off, x32, xb, qkv, attn, h32, ffn, total;
+};
+
+PredictLayout predict_layout(const elis_config& c, int T, int n) {
+    PredictLayout p{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += align_up(bytes);
+        return at;
+    };
+    const size_t d = c.d_model, F = c.d_ff, t = T;
+    p.status = take(sizeof(uint32_t));
+    p.start = take(sizeof(int32_t) * n);
+    p.len = take(sizeof(int32_t) * n);
+    p.tile_off = take(sizeof(int32_t) * (n + 1));
+    p.x32 = take(4 * t * d);
+    if (c.n_layers > 0) {
+        p.xb = take(2 * t * d);
+        p.qkv = take(2 * t * 3 * d);
+        p.attn = take(2 * t * d);
+        p.h32 = take(4 * t * d);
+        p.ffn = take(2 * t * F);
+    }
+    p.total = o;
+    return p;
+}
+
+size_t attention_ws(int n) {
+    return align_up(sizeof(uint32_t)) + 2 * align_up(sizeof(int32_t) * n) + align_up(sizeof(int32_t) * (n + 1));
+}
+
+template <class T>
+T* at(void* base, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t elis_abi_version(void) { return 1; }
+
+const char* elis_status_string(int s) {
+    switch (s) {
+        case ELIS_OK: return "ELIS_OK";
+        case ELIS_EINVAL: return "ELIS_EINVAL: invalid argument";
+        case ELIS_ESHAPE: return "ELIS_ESHAPE: inconsistent sizes";
+        case ELIS_EWORKSPACE: return "ELIS_EWORKSPACE: workspace too small";
+        case ELIS_EHIP: return "ELIS_EHIP: HIP runtime error";
+        case ELIS_EDEVICE: return "ELIS_EDEVICE: device-detected content error";
+        case ELIS_EUNSUPPORTED: return "ELIS_EUNSUPPORTED: shape not supported by this build";
+        default: return "unknown status";
+    }
+}
+
+size_t elis_predict_workspace_bytes(const elis_config* cfg, int32_t total_tokens, int32_t n_seqs,
+                                    int32_t max_seqlen) {
+    if (check_config(cfg) != ELIS_OK || n_seqs <= 0 || total_tokens < n_seqs || max_seqlen < 1 ||
+        max_seqlen > cfg->max_pos)
+        return 0;
+    return predict_layout(*cfg, total_tokens, n_seqs).total;
+}
+
+int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, const int32_t* cu_seqlens,
+                           int32_t n_seqs, int32_t total_tokens, int32_t max_seqlen, float* out_pred,
+                           float* out_hidden, void* workspace, size_t ws_bytes, void* stream) {
+    int r = check_weights(w);
+    if (r != ELIS_OK) return r;
+    if (!token_ids || !cu_seqlens || !out_pred || !workspace) return ELIS_EINVAL;
+    if (n_seqs <= 0 || total_tokens <= 0) return ELIS_EINVAL;
+    if (!aligned(workspace)) return ELIS_EINVAL;
+    const elis_config& c = w->cfg;
+    if (max_seqlen < 1 || max_seqlen > c.max_pos || total_tokens < n_seqs) return ELIS_ESHAPE;
+    const PredictLayout p = predict_layout(c, total_tokens, n_seqs);
+    if (ws_bytes < p.total) return ELIS_EWORKSPACE;
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int T = total_tokens, n = n_seqs, d = c.d_model, F = c.d_ff, L = c.n_layers;
+    uint32_t* status = at<uint32_t>(workspace, p.status);
+    const SeqTable tab{at<int32_t>(workspace, p.start), at<int32_t>(workspace, p.len),
+                       at<int32_t>(workspace, p.tile_off)};
+    float* x32 = at<float>(workspace, p.x32);
+    float* final32 = out_hidden ? out_hidden : x32;
+    uint16_t* xb = L ? at<uint16_t>(workspace, p.xb) : nullptr;
+    uint16_t* qkv = L ? at<uint16_t>(workspace, p.qkv) : nullptr;
+    uint16_t* attn = L ? at<uint16_t>(workspace, p.attn) : nullptr;
+    float* h32 = L ? at<float>(workspace, p.h32) : nullptr;
+    uint16_t* ffn = L ? at<uint16_t>(workspace, p.ffn) : nullptr;
+
+    hipError_t e;
+    e = timed(ELIS_K_SEQMAP, st, [&] { return launch_seqmap(cu_seqlens, n, T, max_seqlen, tab, status, st); });
+    if (e != hipSuccess) return status_of(e);
+    e = timed(ELIS_K_EMBED_LN, st, [&] {
+        return launch_embed_ln(token_ids, cu_seqlens, n, T, w->word, w->pos, w->type0, w->emb_ln_g, w->emb_ln_b, d,
+                               c.vocab, c.max_pos, c.ln_eps, L ? x32 : final32, xb, status, st);
+    });
+    if (e != hipSuccess) return status_of(e);
+    for (int l = 0; l < L; ++l) {
+        const elis_layer_weights& y = w->layers[l];
+        const bool last = (l == L - 1);
+        e = timed(ELIS_K_GEMM_QKV, st, [&] {
+            return launch_gemm(xb, y.w_qkv, y.b_qkv, nullptr, T, 3 * d, d, ELIS_EPI_BIAS_BF16, qkv, st);
+        });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_ATTENTION, st,
+                  [&] { return launch_attention(qkv, tab, n, T, c.n_heads, d / c.n_heads, attn, st); });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_GEMM_O, st, [&] {
+            return launch_gemm(attn, y.w_o, y.b_o, x32, T, d, d, ELIS_EPI_BIAS_RES_F32, h32, st);
+        });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_LAYERNORM, st,
+                  [&] { return launch_layernorm(h32, y.ln1_g, y.ln1_b, T, d, c.ln_eps, x32, xb, st); });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_GEMM_FFN1, st, [&] {
+            return launch_gemm(xb, y.w_1, y.b_1, nullptr, T, F, d, ELIS_EPI_BIAS_GELU_BF16, ffn, st);
+        });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_GEMM_FFN2, st, [&] {
+            return launch_gemm(ffn, y.w_2, y.b_2, x32, T, d, F, ELIS_EPI_BIAS_RES_F32, h32, st, true);
+        });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_LAYERNORM, st, [&] {
+            return launch_layernorm(h32, y.ln2_g, y.ln2_b, T, d, c.ln_eps, last ? final32 : x32,
+                                    last ? nullptr : xb, st);
+        });
+        if (e != hipSuccess) return status_of(e);
+    }
+    e = timed(ELIS_K_POOL_HEAD, st, [&] {
+        return launch_pool_head(final32, tab, n, d, c.pooling, c.head_hidden, w->head_w1, w->head_b1, w->head_w2,
+                                w->head_b2, c.out_scale, c.out_shift, out_pred, st);
+    });
+    return status_of(e);
+}
+
+int32_t elis_select_max_n(void) { return select_max_n(); }
+
+size_t elis_select_workspace_bytes(int32_t n) {
+    if (n < 1 || n > select_max_n()) return 0;
+    return align_up(sizeof(uint32_t));
+}
+
+int elis_isrtf_select(const float* pred, const int64_t* arrival_seq, int32_t n, int32_t batch_cap,
+                      int32_t* out_idx, int32_t* out_count, void* workspace, size_t ws_bytes, void* stream) {
+    if (!pred || !arrival_seq || !out_count || !workspace || (batch_cap > 0 && !out_idx)) return ELIS_EINVAL;
+    if (n <= 0 || batch_cap < 0) return ELIS_EINVAL;
+    if (!aligned(workspace)) return ELIS_EINVAL;
+    if (n > select_max_n()) return ELIS_ESHAPE;
+    if (ws_bytes < elis_select_workspace_bytes(n)) return ELIS_EWORKSPACE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = timed(ELIS_K_SELECT, st, [&] {
+        return launch_select(pred, arrival_seq, n, batch_cap, out_idx, out_count, static_cast<uint32_t*>(workspace),
+                             st);
+    });
+    return status_of(e);
+}
+
+int elis_read_status(const void* workspace, void* stream, uint32_t* bits) {
+    if (!workspace) return ELIS_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (hipStreamSynchronize(st) != hipSuccess) return ELIS_EHIP;
+    uint32_t v = 0;
+    if (hipMemcpy(&v, workspace, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return ELIS_EHIP;
+    if (bits) *bits = v;
+    return v ? ELIS_EDEVICE : ELIS_OK;
+}
+
+int elis_linear(const uint16_t* x, const uint16_t* w, const float* bias, const float* residual, int32_t m, int32_t n,
+                int32_t k, int32_t epilogue, void* out, void* stream) {
+    if (!x || !w || !bias || !out) return ELIS_EINVAL;
+    if (epilogue != ELIS_EPI_BIAS_BF16 && epilogue != ELIS_EPI_BIAS_GELU_BF16 && epilogue != ELIS_EPI_BIAS_RES_F32)
+        return ELIS_EINVAL;
+    if (epilogue == ELIS_EPI_BIAS_RES_F32 && !residual) return ELIS_EINVAL;
+    if (m <= 0 || n <= 0 || k <= 0) return ELIS_EINVAL;
+    if (n % 64 || k % 64) return ELIS_EUNSUPPORTED;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int cls = epilogue == ELIS_EPI_BIAS_GELU_BF16 ? ELIS_K_GEMM_FFN1
+                    : epilogue == ELIS_EPI_BIAS_RES_F32 ? ELIS_K_GEMM_FFN2
+                                                        : ELIS_K_GEMM_QKV;
+    return status_of(timed(cls, st, [&] { return launch_gemm(x, w, bias, residual, m, n, k, epilogue, out, st); }));
+}
+
+size_t elis_attention_workspace_bytes(int32_t n_seqs, int32_t total_tokens) {
+    if (n_seqs <= 0 || total_tokens < n_seqs) return 0;
+    return attention_ws(n_seqs);
+}
+
+int elis_attention(const uint16_t* qkv, const int32_t* cu_seqlens, int32_t n_seqs, int32_t total_tokens,
+                   int32_t max_seqlen, int32_t n_heads, int32_t d_head, uint16_t* out, void* workspace,
+                   size_t ws_bytes, void* stream) {
+    if (!qkv || !cu_seqlens || !out || !workspace) return ELIS_EINVAL;
+    if (n_seqs <= 0 || total_tokens <= 0 || n_heads <= 0 || d_head <= 0) return ELIS_EINVAL;
+    if (!aligned(workspace)) return ELIS_EINVAL;
+    if (d_head != 32 && d_head != 64) return ELIS_EUNSUPPORTED;
+    if (total_tokens < n_seqs || max_seqlen < 1) return ELIS_ESHAPE;
+    if (ws_bytes < attention_ws(n_seqs)) return ELIS_EWORKSPACE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    size_t o = 0;
+    uint32_t* status = at<uint32_t>(workspace, o);
+    o += align_up(sizeof(uint32_t));
+    SeqTable tab;
+    tab.start = at<int32_t>(workspace, o);
+    o += align_up(sizeof(int32_t) * n_seqs);
+    tab.len = at<int32_t>(workspace, o);
+    o += align_up(sizeof(int32_t) * n_seqs);
+    tab.tile_off = at<int32_t>(workspace, o);
+    hipError_t e = timed(ELIS_K_SEQMAP, st,
+                         [&] { return launch_seqmap(cu_seqlens, n_seqs, total_tokens, max_seqlen, tab, status, st); });
+    if (e != hipSuccess) return status_of(e);
+    return status_of(timed(ELIS_K_ATTENTION, st, [&] {
+        return launch_attention(qkv, tab, n_seqs, total_tokens, n_heads, d_head, out, st);
+    }));
+}
+
+int elis_layernorm(const float* x, const float* g, const float* b, int32_t rows, int32_t d, float eps,
+                   float* out_f32, uint16_t* out_bf16, void* stream) {
+    if (!x || !g || !b || (!out_f32 && !out_bf16)) return ELIS_EINVAL;
+    if (rows <= 0 || d <= 0 || !(eps >= 0.f)) return ELIS_EINVAL;
+    if (d % 64 || d > 2048) return ELIS_EUNSUPPORTED;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return status_of(
+        timed(ELIS_K_LAYERNORM, st, [&] { return launch_layernorm(x, g, b, rows, d, eps, out_f32, out_bf16, st); }));
+}
+
+int elis_timing_enable(uint32_t class_mask) {
+    g_timing_mask = class_mask & ((1u << ELIS_K_COUNT) - 1);
+    return ELIS_OK;
+}
+
+int elis_timing_reset(void) {
+    for (auto& t : g_pending) {
+        hipEventSynchronize(t.b);
+        g_free_events.push_back(t.a);
+        g_free_events.push_back(t.b);
+    }
+    g_pending.clear();
+    for (int i = 0; i < ELIS_K_COUNT; ++i) {
+        g_ms[i] = 0.0;
+        g_count[i] = 0;
+    }
+    return ELIS_OK;
+}
+
+int elis_timing_read(int32_t kernel_class, int32_t* launches, double* total_ms) {
+    if (kernel_class < 0 || kernel_class >= ELIS_K_COUNT || !launches || !total_ms) return ELIS_EINVAL;
+    for (auto& t : g_pending) {
+        if (hipEventSynchronize(t.b) != hipSuccess) return ELIS_EHIP;
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, t.a, t.b) != hipSuccess) return ELIS_EHIP;
+        g_ms[t.cls] += ms;
+        g_count[t.cls] += 1;
+        g_free_events.push_back(t.a);
+        g_free_events.push_back(t.b);
+    }
+    g_pending.clear();
+    *launches = g_count[kernel_class];
+    *total_ms = g_ms[kernel_class];
+    return ELIS_OK;
+}
+
+}  // extern "C"

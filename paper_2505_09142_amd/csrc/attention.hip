@@ -1,0 +1,245 @@
+// Variable-length bidirectional multi-head attention over a packed batch
+// (the encoder's self-attention: every token of a sequence attends to every
+// token of the same sequence, and to nothing else).
+//
+// Work decomposition. A work-group takes one (sequence, head, 128-query tile);
+// the tile table built by the seq-map kernel maps blockIdx.x to its sequence.
+// Each of the 4 waves owns 32 queries (two 16-query MFMA blocks) and streams
+// the sequence's keys and values through LDS in 64-token tiles, keeping a
+// running maximum and running sum per query (online softmax), so the score
+// matrix never leaves registers.
+//
+// Transposed formulation. The scores are computed as S^T = K Q^T and the
+// output as O^T = V^T P^T on v_mfma_f32_16x16x32_bf16. With that order every
+// lane holds, for ONE query (its lane % 16), four consecutive keys of each
+// 16-key block in the accumulator layout; those accumulators, rounded to bf16,
+// are directly the lane's slice of the P^T operand of the second product (the
+// 8 k-slots of lane group g are keys {4g..4g+3} and {16+4g..16+4g+3} of a
+// 32-key chunk). The row maximum and row sum of a query are therefore a
+// reduction over the lane's own registers plus two cross-lane shuffles
+// (lanes l, l^16, l^32, l^48 share a query).
+//
+// LDS. K is stored row-major with 16-byte chunks XOR-swizzled by row; V is
+// stored transposed (V^T[d][key], rows padded to 72 keys) so that a lane's
+// 8 keys for one d are two 8-byte reads.
+#include <math.h>
+
+#include "kernels.h"
+
+namespace elis {
+
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kQPerWave = 32;
+constexpr int kBQ = kWaves * kQPerWave;  // == kAttnRowsPerBlock
+constexpr int kBKV = 64;
+constexpr int kVtStride = kBKV + 8;
+static_assert(kBQ == kAttnRowsPerBlock, "tile table and kernel must agree");
+
+template <int DH>
+__device__ __forceinline__ int kswz(int row) {
+    // chunks per K row: DH/8 (8 for d_head 64, 4 for 32)
+    constexpr int CPR = DH / 8;
+    return CPR == 8 ? (row & 7) : ((row >> 1) & 3);
+}
+
+template <int DH>
+__global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t* __restrict__ qkv,
+                                                                  const int32_t* __restrict__ seq_start,
+                                                                  const int32_t* __restrict__ seq_len,
+                                                                  const int32_t* __restrict__ tile_off, int n,
+                                                                  int H, uint16_t* __restrict__ out,
+                                                                  float scale_log2) {
+    constexpr int CPR = DH / 8;   // 16-byte chunks per head row
+    constexpr int KS = DH / 32;   // MFMA k-steps over d_head
+    constexpr int DT = DH / 16;   // 16-wide d blocks of the output
+    __shared__ __attribute__((aligned(16))) uint16_t sK[kBKV * DH];
+    __shared__ __attribute__((aligned(16))) uint16_t sVt[DH * kVtStride];
+
+    const int tile = blockIdx.x, h = blockIdx.y;
+    if (tile >= tile_off[n]) return;  // uniform over the work-group
+    const int s = find_segment(tile_off, n, tile);
+    const int seq0 = seq_start[s], L = seq_len[s];
+    const int q0 = (tile - tile_off[s]) * kBQ;
+
+    const int D = H * DH, D3 = 3 * D;
+    const uint16_t* Qg = qkv + h * DH;
+    const uint16_t* Kg = qkv + D + h * DH;
+    const uint16_t* Vg = qkv + 2 * D + h * DH;
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int g = lane >> 4, r16 = lane & 15;
+    const int qw = q0 + wid * kQPerWave;
+
+    // Query fragments (B operand of S^T = K Q^T): lane holds Q[query][8 d's of its k-group].
+    bf16x8 qf[2][KS];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        int qi = qw + j * 16 + r16;
+        qi = qi < L ? qi : L - 1;
+        const uint16_t* row = Qg + static_cast<size_t>(seq0 + qi) * D3;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[j][ks] = *reinterpret_cast<const bf16x8*>(row + ks * 32 + 8 * g);
+    }
+
+    f32x4 o[DT][2];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) o[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run[2] = {-INFINITY, -INFINITY};
+    float l_run[2] = {0.f, 0.f};
+
+    for (int kv0 = 0; kv0 < L; kv0 += kBKV) {
+        // K tile -> LDS, row-major, swizzled chunks.
+        for (int c = tid; c < kBKV * CPR; c += kWaves * kWave) {
+            const int row = c / CPR, ch = c % CPR;
+            int tok = kv0 + row;
+            tok = tok < L ? tok : L - 1;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(Kg + static_cast<size_t>(seq0 + tok) * D3 + ch * 8);
+            *reinterpret_cast<u32x4*>(&sK[row * DH + ((ch ^ kswz<DH>(row)) * 8)]) = v;
+        }
+        // V tile -> LDS transposed; a thread moves 2 keys x 8 d.
+        for (int u = tid; u < (kBKV / 2) * CPR; u += kWaves * kWave) {
+            const int tp = u % (kBKV / 2), ch = u / (kBKV / 2);
+            int t0 = kv0 + 2 * tp, t1 = t0 + 1;
+            t0 = t0 < L ? t0 : L - 1;
+            t1 = t1 < L ? t1 : L - 1;
+            const u32x4 a = *reinterpret_cast<const u32x4*>(Vg + static_cast<size_t>(seq0 + t0) * D3 + ch * 8);
+            const u32x4 b = *reinterpret_cast<const u32x4*>(Vg + static_cast<size_t>(seq0 + t1) * D3 + ch * 8);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t lo = (a[e] & 0xffffu) | (b[e] << 16);
+                const uint32_t hi = (a[e] >> 16) | (b[e] & 0xffff0000u);
+                *reinterpret_cast<uint32_t*>(&sVt[(ch * 8 + 2 * e) * kVtStride + 2 * tp]) = lo;
+                *reinterpret_cast<uint32_t*>(&sVt[(ch * 8 + 2 * e + 1) * kVtStride + 2 * tp]) = hi;
+            }
+        }
+        __syncthreads();
+
+        // S^T = K Q^T: 4 key blocks x 2 query blocks.
+        f32x4 sc[4][2];
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+            const int row = tt * 16 + r16;
+            bf16x8 kf[KS];
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const int ch = ks * 4 + g;
+                kf[ks] = *reinterpret_cast<const bf16x8*>(&sK[row * DH + ((ch ^ kswz<DH>(row)) * 8)]);
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks], qf[j][ks], a, 0, 0, 0);
+                sc[tt][j] = a;
+            }
+        }
+
+        // Online softmax (base 2; scale_log2 = log2(e) / sqrt(d_head)); keys past the end are masked.
+        const int valid = L - kv0;
+        bf16x8 pf[2][2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int key = tt * 16 + 4 * g + r;
+                    const float x = key < valid ? sc[tt][j][r] * scale_log2 : -INFINITY;
+                    sc[tt][j][r] = x;
+                    mx = fmaxf(mx, x);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+            const float m_new = fmaxf(m_run[j], mx);
+            const float alpha = exp2f(m_run[j] - m_new);
+            m_run[j] = m_new;
+            float rs = 0.f;
+            float p[4][4];
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    p[tt][r] = exp2f(sc[tt][j][r] - m_new);
+                    rs += p[tt][r];
+                }
+            l_run[j] = l_run[j] * alpha + rs;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[dt][j] *= alpha;
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                bf16x8 f;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    f[r] = static_cast<__bf16>(p[2 * kc][r]);
+                    f[4 + r] = static_cast<__bf16>(p[2 * kc + 1][r]);
+                }
+                pf[kc][j] = f;
+            }
+        }
+
+        // O^T += V^T P^T.
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            const int d = dt * 16 + r16;
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const u32x2 lo = *reinterpret_cast<const u32x2*>(&sVt[d * kVtStride + kc * 32 + 4 * g]);
+                const u32x2 hi = *reinterpret_cast<const u32x2*>(&sVt[d * kVtStride + kc * 32 + 16 + 4 * g]);
+                u32x4 w;
+                w[0] = lo[0];
+                w[1] = lo[1];
+                w[2] = hi[0];
+                w[3] = hi[1];
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, w);
+#pragma unroll
+                for (int j = 0; j < 2; ++j) o[dt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc][j], o[dt][j], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+
+    // Normalise and store: lane holds O[query j*16 + r16][d = dt*16 + 4g .. +3].
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        float l = l_run[j];
+        l += __shfl_xor(l, 16, kWave);
+        l += __shfl_xor(l, 32, kWave);
+        const float inv = 1.0f / l;
+        const int qi = qw + j * 16 + r16;
+        if (qi >= L) continue;
+        uint16_t* orow = out + static_cast<size_t>(seq0 + qi) * D + h * DH;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+            u32x2 pk;
+            pk[0] = pack_bf16x2(o[dt][j][0] * inv, o[dt][j][1] * inv);
+            pk[1] = pack_bf16x2(o[dt][j][2] * inv, o[dt][j][3] * inv);
+            *reinterpret_cast<u32x2*>(orow + dt * 16 + 4 * g) = pk;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh, uint16_t* out,
+                            hipStream_t st) {
+    // Upper bound of sum_s ceil(len_s / kBQ); surplus work-groups exit at once.
+    const int tiles = (total + kBQ - 1) / kBQ + n;
+    const dim3 grid(tiles, heads), block(kWaves * kWave);
+    const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
+    if (dh == 64)
+        hipLaunchKernelGGL(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
+                           out, scale_log2);
+    else if (dh == 32)
+        hipLaunchKernelGGL(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
+                           out, scale_log2);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+}  // namespace elis

@@ -1,0 +1,40 @@
+// Host-side launchers of the libelis kernels (each defined in its own .hip file).
+#pragma once
+
+#include "common.h"
+
+namespace elis {
+
+// seqmap.hip: validate cu_seqlens, write the sanitised sequence table and the
+// attention tile prefix; overwrites *status with the ELIS_DEV_* bits found.
+hipError_t launch_seqmap(const int32_t* cu, int n, int total, int max_seqlen, SeqTable tab,
+                         uint32_t* status, hipStream_t st);
+
+// norm.hip
+hipError_t launch_embed_ln(const int32_t* ids, const int32_t* cu, int n, int total,
+                           const uint16_t* word, const uint16_t* pos, const float* type0,
+                           const float* g, const float* b, int d, int vocab, int max_pos, float eps,
+                           float* out32, uint16_t* out16, uint32_t* status, hipStream_t st);
+hipError_t launch_layernorm(const float* x, const float* g, const float* b, int rows, int d, float eps,
+                            float* out32, uint16_t* out16, hipStream_t st);
+
+// gemm.hip
+// ffn2 selects a separately named instantiation of the residual epilogue (profiling only).
+hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m,
+                       int n, int k, int epi, void* out, hipStream_t st, bool ffn2 = false);
+
+// attention.hip
+hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh,
+                            uint16_t* out, hipStream_t st);
+
+// pool_head.hip
+hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int pooling, int head_hidden,
+                            const float* w1, const float* b1, const float* w2, const float* b2,
+                            float scale, float shift, float* out, hipStream_t st);
+
+// select.hip
+int select_max_n();
+hipError_t launch_select(const float* pred, const int64_t* arrival, int n, int k, int32_t* out_idx,
+                         int32_t* out_count, uint32_t* status, hipStream_t st);
+
+}  // namespace elis

@@ -1,0 +1,157 @@
+// Row-wise kernels bound by HBM bandwidth: the fused embedding + LayerNorm and
+// the LayerNorm that closes each post-LN sub-block.
+//
+// One wave per row; each lane owns float4 groups at columns 4*(lane + 64*i),
+// so a wave reads a row in fully coalesced 1 KiB sweeps. Mean and variance are
+// two-pass over the registers (no E[x^2] - E[x]^2 cancellation), reduced with
+// cross-lane shuffles.
+#include "kernels.h"
+
+namespace elis {
+
+namespace {
+
+constexpr int kRowsPerBlock = 4;  // 4 waves, one row each
+
+template <int VPL>
+__device__ __forceinline__ void ln_finish(f32x4 (&v)[VPL], int lane, int d, const float* __restrict__ g,
+                                          const float* __restrict__ b, float eps, float* __restrict__ o32,
+                                          uint16_t* __restrict__ o16) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+        const int e = 4 * (lane + kWave * i);
+        if (e < d) s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+    }
+    const float inv_d = 1.0f / static_cast<float>(d);
+    const float mean = wave_sum(s) * inv_d;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+        const int e = 4 * (lane + kWave * i);
+        if (e < d) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float t = v[i][c] - mean;
+                q += t * t;
+            }
+        }
+    }
+    const float var = wave_sum(q) * inv_d;
+    const float rstd = 1.0f / sqrtf(var + eps);
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+        const int e = 4 * (lane + kWave * i);
+        if (e < d) {
+            const f32x4 gv = *reinterpret_cast<const f32x4*>(g + e);
+            const f32x4 bv = *reinterpret_cast<const f32x4*>(b + e);
+            f32x4 y;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) y[c] = (v[i][c] - mean) * rstd * gv[c] + bv[c];
+            if (o32) *reinterpret_cast<f32x4*>(o32 + e) = y;
+            if (o16) {
+                u32x2 p;
+                p[0] = pack_bf16x2(y[0], y[1]);
+                p[1] = pack_bf16x2(y[2], y[3]);
+                *reinterpret_cast<u32x2*>(o16 + e) = p;
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ f32x4 load_bf16x4(const uint16_t* p) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(p);
+    f32x4 r;
+    r[0] = __uint_as_float(w[0] << 16);
+    r[1] = __uint_as_float(w[0] & 0xffff0000u);
+    r[2] = __uint_as_float(w[1] << 16);
+    r[3] = __uint_as_float(w[1] & 0xffff0000u);
+    return r;
+}
+
+template <int VPL>
+__global__ __launch_bounds__(kRowsPerBlock* kWave) void embed_ln_kernel(
+    const int32_t* __restrict__ ids, const int32_t* __restrict__ cu, int n, int total,
+    const uint16_t* __restrict__ word, const uint16_t* __restrict__ pos, const float* __restrict__ type0,
+    const float* __restrict__ g, const float* __restrict__ b, int d, int vocab, int max_pos, float eps,
+    float* __restrict__ out32, uint16_t* __restrict__ out16, uint32_t* __restrict__ status) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int t = blockIdx.x * kRowsPerBlock + (threadIdx.x / kWave);
+    if (t >= total) return;
+    const int s = find_segment(cu, n, t);
+    int p = t - cu[s];
+    p = p < 0 ? 0 : (p >= max_pos ? max_pos - 1 : p);
+    int id = ids[t];
+    if (id < 0 || id >= vocab) {
+        if (lane == 0) atomicOr(status, ELIS_DEV_BAD_TOKEN);
+        id = id < 0 ? 0 : vocab - 1;
+    }
+    const uint16_t* wr = word + static_cast<size_t>(id) * d;
+    const uint16_t* pr = pos + static_cast<size_t>(p) * d;
+    f32x4 v[VPL];
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+        const int e = 4 * (lane + kWave * i);
+        if (e < d) v[i] = load_bf16x4(wr + e) + load_bf16x4(pr + e) + *reinterpret_cast<const f32x4*>(type0 + e);
+    }
+    const size_t off = static_cast<size_t>(t) * d;
+    ln_finish<VPL>(v, lane, d, g, b, eps, out32 ? out32 + off : nullptr, out16 ? out16 + off : nullptr);
+}
+
+template <int VPL>
+__global__ __launch_bounds__(kRowsPerBlock* kWave) void layernorm_kernel(const float* __restrict__ x,
+                                                                         const float* __restrict__ g,
+                                                                         const float* __restrict__ b, int rows,
+                                                                         int d, float eps, float* __restrict__ o32,
+                                                                         uint16_t* __restrict__ o16) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x / kWave);
+    if (r >= rows) return;
+    const size_t off = static_cast<size_t>(r) * d;
+    f32x4 v[VPL];
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+        const int e = 4 * (lane + kWave * i);
+        if (e < d) v[i] = *reinterpret_cast<const f32x4*>(x + off + e);
+    }
+    ln_finish<VPL>(v, lane, d, g, b, eps, o32 ? o32 + off : nullptr, o16 ? o16 + off : nullptr);
+}
+
+}  // namespace
+
+#define ELIS_VPL_SWITCH(d, CALL)          \
+    switch ((d + 255) / 256) {            \
+        case 1: CALL(1); break;           \
+        case 2: CALL(2); break;           \
+        case 3: CALL(3); break;           \
+        case 4: CALL(4); break;           \
+        case 5: CALL(5); break;           \
+        case 6: CALL(6); break;           \
+        case 7: CALL(7); break;           \
+        case 8: CALL(8); break;           \
+        default: return hipErrorInvalidValue; \
+    }
+
+hipError_t launch_embed_ln(const int32_t* ids, const int32_t* cu, int n, int total, const uint16_t* word,
+                           const uint16_t* pos, const float* type0, const float* g, const float* b, int d,
+                           int vocab, int max_pos, float eps, float* out32, uint16_t* out16, uint32_t* status,
+                           hipStream_t st) {
+    const dim3 grid((total + kRowsPerBlock - 1) / kRowsPerBlock), block(kRowsPerBlock * kWave);
+#define CALL(V)                                                                                          \
+    hipLaunchKernelGGL(embed_ln_kernel<V>, grid, block, 0, st, ids, cu, n, total, word, pos, type0, g, b, d, \
+                       vocab, max_pos, eps, out32, out16, status)
+    ELIS_VPL_SWITCH(d, CALL)
+#undef CALL
+    return hipGetLastError();
+}
+
+hipError_t launch_layernorm(const float* x, const float* g, const float* b, int rows, int d, float eps,
+                            float* out32, uint16_t* out16, hipStream_t st) {
+    const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock), block(kRowsPerBlock * kWave);
+#define CALL(V) hipLaunchKernelGGL(layernorm_kernel<V>, grid, block, 0, st, x, g, b, rows, d, eps, out32, out16)
+    ELIS_VPL_SWITCH(d, CALL)
+#undef CALL
+    return hipGetLastError();
+}
+
+}  // namespace elis

@@ -1,0 +1,161 @@
+"""The C-ABI library on the host: it loads, exports every symbol the header
+declares, and rejects invalid arguments with the documented status before
+touching the device (no kernel is launched by any call here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2505_09142_amd import _elis as E
+from workloads import BERT_BASE, TINY, XLMR_LARGE
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "elis.h")
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+FAKE_WS = 0x100000  # 256-byte aligned
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(elis_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(E.LIB_PATH):
+        pytest.fail("libelis.so is not built (run python -m paper_2505_09142_amd.build)")
+    return E.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(E.SIGNATURES), "binding and header disagree"
+
+
+def test_version_and_strings(lib):
+    assert E.elis_abi_version() == 1
+    for s in (0, -1, -2, -3, -4, -5, -6):
+        assert E.elis_status_string(s).startswith("ELIS_")
+    assert E.elis_status_string(123) == "unknown status"
+
+
+def test_workspace_queries(lib):
+    for shape in (TINY, BERT_BASE, XLMR_LARGE):
+        cfg = E.elis_config(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ff, shape.vocab, shape.max_pos,
+                            shape.pooling, shape.head_hidden, shape.ln_eps, shape.out_scale, shape.out_shift)
+        b = E.elis_predict_workspace_bytes(cfg, 1000, 8, 64)
+        d, F = shape.d_model, shape.d_ff
+        # fp32 residual + bf16 copy + qkv + attention out + fp32 pre-LN + FFN activation
+        assert b >= 1000 * (4 * d + 2 * d + 6 * d + 2 * d + 4 * d + 2 * F)
+        assert b % 256 == 0
+        assert E.elis_predict_workspace_bytes(cfg, 7, 8, 64) == 0       # fewer tokens than sequences
+        assert E.elis_predict_workspace_bytes(cfg, 100, 8, shape.max_pos + 1) == 0
+    assert E.elis_select_workspace_bytes(0) == 0
+    assert E.elis_select_workspace_bytes(E.elis_select_max_n() + 1) == 0
+    assert E.elis_select_workspace_bytes(64) >= 4
+    assert E.elis_attention_workspace_bytes(4, 100) > 0
+    assert E.elis_attention_workspace_bytes(4, 3) == 0
+
+
+def _weights(shape=TINY):
+    cfg = E.elis_config(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ff, shape.vocab, shape.max_pos,
+                        shape.pooling, shape.head_hidden, shape.ln_eps, shape.out_scale, shape.out_shift)
+    layers = (E.elis_layer_weights * max(1, shape.n_layers))()
+    for l in range(shape.n_layers):
+        for f, _ in E.elis_layer_weights._fields_:
+            setattr(layers[l], f, FAKE)
+    w = E.elis_weights(cfg, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.cast(layers, ctypes.POINTER(E.elis_layer_weights)),
+                       FAKE, FAKE, FAKE, FAKE)
+    w._keep = layers
+    return w
+
+
+def _predict(w, ids=FAKE, cu=FAKE, n=4, T=100, max_seqlen=64, pred=FAKE, ws=FAKE_WS, wsb=1 << 40):
+    return E.elis_predict_remaining(w, ids, cu, n, T, max_seqlen, pred, None, ws, wsb, None)
+
+
+def test_predict_rejects_invalid_arguments(lib):
+    w = _weights()
+    assert _predict(None) == E.ELIS_EINVAL
+    assert _predict(w, ids=None) == E.ELIS_EINVAL
+    assert _predict(w, cu=None) == E.ELIS_EINVAL
+    assert _predict(w, pred=None) == E.ELIS_EINVAL
+    assert _predict(w, ws=None) == E.ELIS_EINVAL
+    assert _predict(w, ws=FAKE_WS + 8) == E.ELIS_EINVAL          # misaligned workspace
+    assert _predict(w, n=0) == E.ELIS_EINVAL
+    assert _predict(w, n=-3) == E.ELIS_EINVAL
+    assert _predict(w, T=0) == E.ELIS_EINVAL
+    assert _predict(w, max_seqlen=TINY.max_pos + 1) == E.ELIS_ESHAPE
+    assert _predict(w, max_seqlen=0) == E.ELIS_ESHAPE
+    assert _predict(w, n=8, T=5) == E.ELIS_ESHAPE
+    assert _predict(w, wsb=1000) == E.ELIS_EWORKSPACE
+
+
+def test_predict_rejects_bad_config(lib):
+    w = _weights()
+    w.cfg.pooling = 7
+    assert _predict(w) == E.ELIS_EINVAL
+    w = _weights()
+    w.cfg.d_model = 96                                           # not a multiple of 64
+    assert _predict(w) == E.ELIS_EUNSUPPORTED
+    w = _weights()
+    w.cfg.n_heads = 1                                            # d_head 128
+    assert _predict(w) == E.ELIS_EUNSUPPORTED
+    w = _weights()
+    w.cfg.ln_eps = float("nan")
+    assert _predict(w) == E.ELIS_EINVAL
+    w = _weights()
+    w.layers[1].w_2 = None
+    assert _predict(w) == E.ELIS_EINVAL
+    w = _weights()
+    w.cfg.head_hidden = 16
+    w.head_w1 = None
+    assert _predict(w) == E.ELIS_EINVAL
+
+
+def test_select_rejects_invalid_arguments(lib):
+    ok = dict(pred=FAKE, arr=FAKE, n=8, k=4, idx=FAKE, cnt=FAKE, ws=FAKE_WS, wsb=256)
+
+    def call(**kw):
+        a = {**ok, **kw}
+        return E.elis_isrtf_select(a["pred"], a["arr"], a["n"], a["k"], a["idx"], a["cnt"], a["ws"], a["wsb"], None)
+
+    assert call(pred=None) == E.ELIS_EINVAL
+    assert call(arr=None) == E.ELIS_EINVAL
+    assert call(cnt=None) == E.ELIS_EINVAL
+    assert call(idx=None) == E.ELIS_EINVAL
+    assert call(n=0) == E.ELIS_EINVAL
+    assert call(k=-1) == E.ELIS_EINVAL
+    assert call(ws=FAKE_WS + 4) == E.ELIS_EINVAL
+    assert call(n=E.elis_select_max_n() + 1) == E.ELIS_ESHAPE
+    assert call(wsb=0) == E.ELIS_EWORKSPACE
+
+
+def test_building_blocks_reject_invalid_arguments(lib):
+    assert E.elis_linear(None, FAKE, FAKE, None, 4, 64, 64, 0, FAKE, None) == E.ELIS_EINVAL
+    assert E.elis_linear(FAKE, FAKE, FAKE, None, 4, 64, 64, 2, FAKE, None) == E.ELIS_EINVAL  # residual missing
+    assert E.elis_linear(FAKE, FAKE, FAKE, None, 4, 64, 64, 9, FAKE, None) == E.ELIS_EINVAL
+    assert E.elis_linear(FAKE, FAKE, FAKE, None, 0, 64, 64, 0, FAKE, None) == E.ELIS_EINVAL
+    assert E.elis_linear(FAKE, FAKE, FAKE, None, 4, 96, 64, 0, FAKE, None) == E.ELIS_EUNSUPPORTED
+    assert E.elis_linear(FAKE, FAKE, FAKE, None, 4, 64, 80, 0, FAKE, None) == E.ELIS_EUNSUPPORTED
+    assert E.elis_attention(FAKE, FAKE, 2, 10, 8, 2, 48, FAKE, FAKE_WS, 4096, None) == E.ELIS_EUNSUPPORTED
+    assert E.elis_attention(FAKE, FAKE, 2, 1, 8, 2, 64, FAKE, FAKE_WS, 4096, None) == E.ELIS_ESHAPE
+    assert E.elis_attention(FAKE, FAKE, 2, 10, 8, 2, 64, FAKE, FAKE_WS, 8, None) == E.ELIS_EWORKSPACE
+    assert E.elis_attention(None, FAKE, 2, 10, 8, 2, 64, FAKE, FAKE_WS, 4096, None) == E.ELIS_EINVAL
+    assert E.elis_layernorm(FAKE, FAKE, FAKE, 4, 64, 1e-5, None, None, None) == E.ELIS_EINVAL
+    assert E.elis_layernorm(FAKE, FAKE, FAKE, 4, 100, 1e-5, FAKE, None, None) == E.ELIS_EUNSUPPORTED
+    assert E.elis_layernorm(FAKE, FAKE, FAKE, 0, 64, 1e-5, FAKE, None, None) == E.ELIS_EINVAL
+
+
+def test_timing_api_host_only(lib):
+    assert E.elis_timing_enable(0) == 0
+    assert E.elis_timing_reset() == 0
+    st, n, ms = E.elis_timing_read(0)
+    assert st == 0 and n == 0 and ms == 0.0
+    assert E.elis_timing_read(99)[0] == E.ELIS_EINVAL

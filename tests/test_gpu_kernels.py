@@ -1,0 +1,220 @@
+"""Per-kernel parity of libelis against the fp64 oracle, through the C ABI.
+
+Tolerances follow from the arithmetic: operands are bf16 (8-bit significand),
+accumulation is fp32, and bf16 outputs carry one final rounding of relative
+size <= 2^-9.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2505_09142_amd import _elis as E
+from tests.gpu_util import bf16_to_f64, dev, host_u16, note, ok, stream, workspace
+from workloads import f32_to_bf16_bits, pack
+
+pytestmark = pytest.mark.gpu
+
+U32 = lambda *v: np.array(v, dtype=np.uint32).view(np.float32)
+SPECIAL_BITS = U32(0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC00000, 0xFFC00000, 0x7F800001,
+                   0xFF812345, 0x00000001, 0x80000001, 0x007FFFFF, 0x807FFFFF, 0x3F800000, 0x3F800000,
+                   0xBF800000, 0x7F7FFFFF, 0xFF7FFFFF)
+
+
+def _preds(kind: str, n: int, rng) -> np.ndarray:
+    if kind == "normal":
+        return (rng.standard_normal(n) * 100 + 250).astype(np.float32)
+    if kind == "ties":
+        return rng.integers(0, 4, size=n).astype(np.float32)
+    if kind == "special":
+        return rng.choice(SPECIAL_BITS, size=n)
+    if kind == "equal":
+        return np.full(n, 7.5, np.float32)
+    raise ValueError(kind)
+
+
+SELECT_CASES = [(n, kind) for n in (1, 2, 8, 64, 255, 256, 1000, 1024) for kind in ("normal", "ties", "special")]
+SELECT_CASES += [(n, kind) for n in (1025, 3000, 4096, 8192) for kind in ("normal", "ties", "special", "equal")]
+SELECT_CASES += [(64, "equal"), (1024, "equal")]
+
+
+@pytest.mark.parametrize("n,kind", SELECT_CASES)
+def test_select_bit_exact(n, kind):
+    rng = np.random.default_rng(n * 7 + len(kind))
+    pred = _preds(kind, n, rng)
+    arr = rng.integers(0, max(2, n // 2), size=n).astype(np.int64)   # repeated arrival values too
+    d_pred, d_arr = dev(pred), dev(arr)
+    buf, ws, wsb = workspace(E.elis_select_workspace_bytes(n))
+    for k in sorted({0, 1, n // 2, n, n + 5}):
+        note(f"select n={n} kind={kind} k={k}")
+        idx = torch.full((max(1, k),), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        ok(E.elis_isrtf_select(d_pred.data_ptr(), d_arr.data_ptr(), n, k, idx.data_ptr(), cnt.data_ptr(), ws, wsb,
+                               stream()), "select")
+        torch.cuda.synchronize()
+        m = min(k, n)
+        assert int(cnt.item()) == m
+        got = idx.cpu().numpy()[:m]
+        exp = oracle.oracle_select(pred, arr, k)
+        assert np.array_equal(got, exp), f"n={n} kind={kind} k={k}"
+        st, bits = E.elis_read_status(ws, stream())
+        assert st == E.ELIS_OK and bits == 0
+
+
+def test_select_worked_example():
+    import json, os
+    cases = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "srtf_two_requests.json")))["cases"]
+    buf, ws, wsb = workspace(256)
+    for c in cases:
+        note(f"select golden: {c['what']}")
+        pred = dev(np.array(c["pred"], np.float32))
+        arr = dev(np.array(c["arrival_seq"], np.int64))
+        idx = torch.full((2,), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+        ok(E.elis_isrtf_select(pred.data_ptr(), arr.data_ptr(), 2, c["batch_cap"], idx.data_ptr(), cnt.data_ptr(),
+                               ws, wsb, stream()))
+        torch.cuda.synchronize()
+        assert idx.cpu().numpy()[:int(cnt.item())].tolist() == c["selected"]
+
+
+# ------------------------------------------------------------------------------ LayerNorm
+
+@pytest.mark.parametrize("rows,d", [(1, 64), (7, 128), (1000, 768), (333, 1024), (65, 2048)])
+def test_layernorm(rows, d):
+    note(f"layernorm rows={rows} d={d}")
+    rng = np.random.default_rng(rows + d)
+    x = (rng.standard_normal((rows, d)) * 3 + 1.5).astype(np.float32)
+    g = (1 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+    b = (0.1 * rng.standard_normal(d)).astype(np.float32)
+    eps = 1e-5
+    o32 = torch.empty((rows, d), dtype=torch.float32, device="cuda")
+    o16 = torch.empty((rows, d), dtype=torch.int16, device="cuda")
+    d_x, d_g, d_b = dev(x), dev(g), dev(b)  # keep the uploads alive until the kernel has run
+    ok(E.elis_layernorm(d_x.data_ptr(), d_g.data_ptr(), d_b.data_ptr(), rows, d, eps, o32.data_ptr(),
+                        o16.data_ptr(), stream()))
+    torch.cuda.synchronize()
+    ref = oracle.layer_norm(x.astype(np.float64), g, b, eps)
+    err32 = np.abs(o32.cpu().numpy() - ref)
+    assert err32.max() < 2e-5 * (1 + np.abs(ref).max()), err32.max()
+    got16 = bf16_to_f64(host_u16(o16))
+    assert np.all(np.abs(got16 - ref) <= 2.0 ** -8 * np.abs(ref) + 2e-5)
+
+
+# ------------------------------------------------------------------------------ GEMM
+
+GEMM_CASES = [(1, 64, 64), (37, 128, 64), (300, 384, 128), (1000, 768, 768), (129, 3072, 768),
+              (517, 768, 3072), (2048, 2304, 768), (77, 192, 256)]
+
+
+@pytest.mark.parametrize("epi", [E.ELIS_EPI_BIAS_BF16, E.ELIS_EPI_BIAS_GELU_BF16, E.ELIS_EPI_BIAS_RES_F32])
+@pytest.mark.parametrize("m,n,k", GEMM_CASES)
+def test_linear(m, n, k, epi):
+    note(f"linear m={m} n={n} k={k} epi={epi}")
+    rng = np.random.default_rng(m * 31 + n + k + epi)
+    xb = f32_to_bf16_bits(rng.standard_normal((m, k)).astype(np.float32))
+    wb = f32_to_bf16_bits((rng.standard_normal((n, k)) * 0.05).astype(np.float32))
+    bias = (rng.standard_normal(n) * 0.1).astype(np.float32)
+    res = rng.standard_normal((m, n)).astype(np.float32)
+    x64, w64 = bf16_to_f64(xb), bf16_to_f64(wb)
+    pre = x64 @ w64.T + bias
+    mag = np.abs(x64) @ np.abs(w64).T                    # bound on fp32 accumulation error scale
+    if epi == E.ELIS_EPI_BIAS_RES_F32:
+        out = torch.empty((m, n), dtype=torch.float32, device="cuda")
+        d_res = dev(res)
+        rp = d_res.data_ptr()
+    else:
+        out = torch.empty((m, n), dtype=torch.int16, device="cuda")
+        rp = None
+    d_x, d_w, d_bias = dev(xb), dev(wb), dev(bias)  # keep the uploads alive until the kernel has run
+    ok(E.elis_linear(d_x.data_ptr(), d_w.data_ptr(), d_bias.data_ptr(), rp, m, n, k, epi,
+                     out.data_ptr(), stream()))
+    torch.cuda.synchronize()
+    acc_tol = 1e-5 * mag + 1e-6
+    if epi == E.ELIS_EPI_BIAS_RES_F32:
+        ref = pre + res
+        got = out.cpu().numpy().astype(np.float64)
+        assert np.all(np.abs(got - ref) <= acc_tol + 1e-6 * np.abs(ref))
+    else:
+        ref = oracle.gelu(pre) if epi == E.ELIS_EPI_BIAS_GELU_BF16 else pre
+        got = bf16_to_f64(host_u16(out))
+        assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1.2 * acc_tol), np.abs(got - ref).max()
+
+
+# ------------------------------------------------------------------------------ attention
+
+ATT_LENS = [
+    [1],
+    [5, 1, 17],
+    [63, 64, 65],
+    [127, 128, 129, 1, 300],
+    [512, 200, 511],
+    [1000, 33],
+]
+
+
+def _attention_case(lens, heads, dh, sharp, seed):
+    rng = np.random.default_rng(seed)
+    T = int(sum(lens))
+    D = heads * dh
+    qkv = rng.standard_normal((T, 3 * D)).astype(np.float32)
+    if sharp:
+        qkv[:, :D] *= 6.0  # peaked softmax: large score gaps
+    qkv_b = f32_to_bf16_bits(qkv)
+    b = pack([np.zeros(L, np.int32) for L in lens])
+    return qkv_b, b, T, D
+
+
+@pytest.mark.parametrize("dh,heads", [(64, 2), (32, 4), (64, 12)])
+@pytest.mark.parametrize("lens", ATT_LENS)
+@pytest.mark.parametrize("sharp", [False, True])
+def test_attention(lens, dh, heads, sharp):
+    note(f"attention lens={lens} dh={dh} heads={heads} sharp={sharp}")
+    qkv_b, b, T, D = _attention_case(lens, heads, dh, sharp, seed=sum(lens) + dh + heads + sharp)
+    n = len(lens)
+    out = torch.empty((T, D), dtype=torch.int16, device="cuda")
+    buf, ws, wsb = workspace(E.elis_attention_workspace_bytes(n, T))
+    d_cu, d_qkv = dev(b.cu_seqlens), dev(qkv_b)
+    ok(E.elis_attention(d_qkv.data_ptr(), d_cu.data_ptr(), n, T, max(lens), heads, dh, out.data_ptr(), ws,
+                        wsb, stream()))
+    st, bits = E.elis_read_status(ws, stream())
+    assert st == E.ELIS_OK and bits == 0
+    got = bf16_to_f64(host_u16(out))
+    q64 = bf16_to_f64(qkv_b)
+    for s in range(n):
+        a, e = b.cu_seqlens[s], b.cu_seqlens[s + 1]
+        q, k, v = q64[a:e, :D], q64[a:e, D:2 * D], q64[a:e, 2 * D:]
+        ref = oracle.self_attention(q, k, v, heads)
+        vmax = np.abs(v).max()
+        err = np.abs(got[a:e] - ref)
+        # P is rounded to bf16 before the P.V product (<= 2^-9 relative per weight) and the
+        # output once more to bf16.
+        assert err.max() <= 2.0 ** -7 * vmax + 2.0 ** -8 * np.abs(ref).max(), (s, err.max())
+
+
+def test_attention_single_token_is_value():
+    note("attention single-token sequences")
+    heads, dh = 2, 64
+    lens = [1] * 9
+    qkv_b, b, T, D = _attention_case(lens, heads, dh, False, 3)
+    out = torch.empty((T, D), dtype=torch.int16, device="cuda")
+    buf, ws, wsb = workspace(E.elis_attention_workspace_bytes(9, T))
+    d_qkv, d_cu = dev(qkv_b), dev(b.cu_seqlens)
+    ok(E.elis_attention(d_qkv.data_ptr(), d_cu.data_ptr(), 9, T, 1, heads, dh, out.data_ptr(), ws,
+                        wsb, stream()))
+    torch.cuda.synchronize()
+    # softmax over one key is exactly 1, so the output is the value row, bit for bit
+    assert np.array_equal(host_u16(out), qkv_b[:, 2 * D:])
+
+
+def test_attention_flags_bad_cu_without_faulting():
+    note("attention with malformed cu_seqlens (clamped, flagged)")
+    heads, dh = 2, 32
+    qkv_b = f32_to_bf16_bits(np.ones((20, 3 * heads * dh), np.float32))
+    cu = np.array([0, 10, 5, 20], np.int32)  # not increasing
+    out = torch.zeros((20, heads * dh), dtype=torch.int16, device="cuda")
+    buf, ws, wsb = workspace(E.elis_attention_workspace_bytes(3, 20))
+    d_qkv, d_cu = dev(qkv_b), dev(cu)
+    ok(E.elis_attention(d_qkv.data_ptr(), d_cu.data_ptr(), 3, 20, 16, heads, dh, out.data_ptr(), ws, wsb,
+                        stream()))
+    st, bits = E.elis_read_status(ws, stream())
+    assert st == E.ELIS_EDEVICE and bits & E.ELIS_DEV_BAD_CU

@@ -1,0 +1,165 @@
+"""End-to-end parity of elis_predict_remaining + elis_isrtf_select against the
+fp64 oracle on the workloads' own seeded inputs.
+
+Bars: predictions within relative 2e-2 (relative to max(|p_oracle|, 1)), final
+hidden states within max-abs 5e-2, and the selection bit-exact when both
+sides see the same fp32 predictions. The oracle is evaluated on every
+sequence for the small shapes and on sampled sequences (shortest, longest and
+random ones) for the full-size shapes, where it needs seconds per sequence.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2505_09142_amd import _elis as E
+from paper_2505_09142_amd.device import DeviceWeights, Predictor, upload_batch
+from tests.gpu_util import dev, note
+from workloads import (TINY, W_BERT_B64, W_TINY, W_XLMR_B128, bf16_bits_to_f32, make_batch, make_weights, pack)
+
+pytestmark = pytest.mark.gpu
+
+PRED_RTOL = 2e-2
+HIDDEN_ATOL = 5e-2
+
+
+_cache = {}
+
+
+def predictor(shape, seed):
+    key = (shape, seed)
+    if key not in _cache:
+        W = make_weights(shape, seed)
+        _cache.clear()
+        _cache[key] = (W, Predictor(DeviceWeights(shape, W.device)))
+    return _cache[key]
+
+
+def run(pr, batch, want_hidden=True):
+    ids, cu, arr = upload_batch(batch)
+    pred, hid = pr.predict(ids, cu, batch.max_seqlen, want_hidden=want_hidden)
+    st, bits = pr.status()
+    assert st == E.ELIS_OK, (st, bits)
+    return pred.cpu().numpy(), (hid.cpu().numpy() if hid is not None else None), arr
+
+
+def rel_err(p, ref):
+    return np.abs(p - ref) / np.maximum(np.abs(ref), 1.0)
+
+
+def check_selection(pr, pred_gpu, d_arr, arr, k, pred_ref=None, err_bound=None):
+    idx, cnt = pr.select(torch.from_numpy(pred_gpu).cuda(), d_arr, k)
+    torch.cuda.synchronize()
+    m = int(cnt.item())
+    got = idx.cpu().numpy()[:m]
+    assert np.array_equal(got, oracle.oracle_select(pred_gpu, arr, k))
+    if pred_ref is not None and len(pred_ref) > k:
+        # end-to-end: the sets can only differ at a near-tie at the cut
+        srt = np.sort(pred_ref)
+        gap = srt[k] - srt[k - 1]
+        if gap > 2 * err_bound:
+            assert np.array_equal(np.sort(got), np.sort(oracle.oracle_select(pred_ref.astype(np.float32), arr, k)))
+
+
+def test_embedding_layernorm_only():
+    note("predict with zero layers (embedding + LayerNorm, pooling, head)")
+    shape = dataclasses.replace(TINY, n_layers=0)
+    W = make_weights(TINY, 1001)
+    pr = Predictor(DeviceWeights(shape, {k: v for k, v in W.device.items()}))
+    b = make_batch(W_TINY)
+    pred, hid, _ = run(pr, b)
+    m = dict(W.master)
+    m["word"] = bf16_bits_to_f32(W.device["word"])   # the device tables are the bf16 roundings
+    m["pos"] = bf16_bits_to_f32(W.device["pos"])
+    ref_p, ref_h = oracle.oracle_forward(b.token_ids, b.cu_seqlens, m, shape)
+    assert np.abs(hid - ref_h).max() < 1e-4
+    assert rel_err(pred, ref_p).max() < 1e-5
+
+
+def test_tiny_end_to_end():
+    note("tiny predictor, all sequences, fp32 master weights in the oracle")
+    W, pr = predictor(W_TINY.shape, W_TINY.weight_seed)
+    b = make_batch(W_TINY)
+    pred, hid, d_arr = run(pr, b)
+    ref_p, ref_h = oracle.oracle_forward(b.token_ids, b.cu_seqlens, W.master, W_TINY.shape)
+    herr = np.abs(hid - ref_h).max()
+    perr = rel_err(pred, ref_p).max()
+    note(f"tiny: hidden max-abs {herr:.3e}, pred max-rel {perr:.3e}")
+    assert herr <= HIDDEN_ATOL and perr <= PRED_RTOL
+    check_selection(pr, pred, d_arr, b.arrival_seq, W_TINY.batch_cap, ref_p,
+                    np.abs(pred - ref_p).max())
+
+
+def _sample(lengths, count, seed):
+    rng = np.random.default_rng(seed)
+    pick = {int(np.argmin(lengths)), int(np.argmax(lengths))}
+    while len(pick) < count:
+        pick.add(int(rng.integers(len(lengths))))
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("w,count", [(W_BERT_B64, 5), (W_XLMR_B128, 3)])
+def test_full_size_sampled(w, count):
+    note(f"{w.name}: GPU on the whole batch, oracle on {count} sampled sequences")
+    W, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    pred, hid, d_arr = run(pr, b)
+    assert np.all(np.isfinite(pred)) and np.all(np.isfinite(hid))
+    seqs = _sample(b.lengths, count, 7)
+    ref_p, ref_h = oracle.oracle_forward(b.token_ids, b.cu_seqlens, W.master, w.shape, seqs=seqs)
+    for s in seqs:
+        a, e = b.cu_seqlens[s], b.cu_seqlens[s + 1]
+        herr = np.abs(hid[a:e] - ref_h[a:e]).max()
+        perr = rel_err(pred[s], ref_p[s])
+        note(f"{w.name} seq {s} len {e - a}: hidden max-abs {herr:.3e}, pred rel {perr:.3e}")
+        assert herr <= HIDDEN_ATOL and perr <= PRED_RTOL
+    check_selection(pr, pred, d_arr, b.arrival_seq, w.batch_cap)
+
+
+def test_deterministic_and_packing_invariant():
+    w = W_BERT_B64
+    W, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    note("bert_base_b64 twice: bitwise equal")
+    p1, h1, _ = run(pr, b)
+    p2, h2, _ = run(pr, b)
+    assert np.array_equal(p1, p2) and np.array_equal(h1, h2)
+    note("bert_base_b64: sequences alone vs packed, bitwise equal")
+    for s in (0, 17, 63):
+        alone = pack([b.seq(s)])
+        pa, ha, _ = run(pr, alone)
+        assert pa[0] == p1[s]
+        assert np.array_equal(ha, h1[b.cu_seqlens[s]:b.cu_seqlens[s + 1]])
+    note("bert_base_b64: permuted batch gives permuted predictions")
+    perm = np.random.default_rng(0).permutation(b.n)
+    bp = pack([b.seq(int(i)) for i in perm])
+    pp, _, _ = run(pr, bp, want_hidden=False)
+    assert np.array_equal(pp, p1[perm])
+
+
+def test_device_content_errors_are_flagged():
+    W, pr = predictor(W_TINY.shape, W_TINY.weight_seed)
+    b = make_batch(W_TINY)
+    cases = []
+    bad_ids = b.token_ids.copy()
+    bad_ids[5] = W_TINY.shape.vocab + 3
+    cases.append(("token id >= vocab", bad_ids, b.cu_seqlens, b.max_seqlen, E.ELIS_DEV_BAD_TOKEN))
+    neg = b.token_ids.copy()
+    neg[0] = -1
+    cases.append(("negative token id", neg, b.cu_seqlens, b.max_seqlen, E.ELIS_DEV_BAD_TOKEN))
+    cu = b.cu_seqlens.copy()
+    cu[3], cu[4] = cu[4], cu[3]
+    cases.append(("cu_seqlens not increasing", b.token_ids, cu, b.max_seqlen, E.ELIS_DEV_BAD_CU))
+    cu0 = b.cu_seqlens.copy()
+    cu0[0] = 2
+    cases.append(("cu_seqlens[0] != 0", b.token_ids, cu0, b.max_seqlen, E.ELIS_DEV_BAD_CU))
+    cases.append(("length above max_seqlen", b.token_ids, b.cu_seqlens, int(b.lengths.min()), E.ELIS_DEV_LONG_SEQ))
+    for what, ids, cu_, msl, bit in cases:
+        note(f"content error: {what}")
+        pred, _ = pr.predict(dev(ids), dev(cu_), msl)
+        st, bits = pr.status()
+        assert st == E.ELIS_EDEVICE and bits & bit, (what, st, bits)
+    note("valid batch after errors: status clears")
+    run(pr, b)
