@@ -53,7 +53,7 @@ def build(verbose: bool = True) -> str:
         f.write("{ global: elis_*; local: *; };\n")
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs,
-           f"-Wl,--version-script={vscript}"]
+           f"-Wl,--version-script={vscript}", "-Wl,--no-undefined"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -91,10 +91,11 @@ bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) =
 
 // ------------------------------------------------------------------ workspace layout
 struct PredictLayout {
-    size_t status, start, len, tile_off, x32, xb, qkv, attn, h32, ffn, total;
+    size_t status, start, len, tile_off, x32, xb, qkv, attn, h32, ffn, pool_partial, pool_z, head_hid, total;
+    int nchunk;
 };
 
-PredictLayout predict_layout(const elis_config& c, int T, int n) {
+PredictLayout predict_layout(const elis_config& c, int T, int n, int max_seqlen) {
     PredictLayout p{};
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -115,6 +116,12 @@ PredictLayout predict_layout(const elis_config& c, int T, int n) {
         p.h32 = take(4 * t * d);
         p.ffn = take(2 * t * F);
     }
+    p.nchunk = (max_seqlen + kPoolChunk - 1) / kPoolChunk;
+    if (c.pooling == ELIS_POOL_MEAN) {
+        p.pool_partial = take(sizeof(float) * static_cast<size_t>(n) * p.nchunk * d);
+        p.pool_z = take(sizeof(float) * static_cast<size_t>(n) * d);
+    }
+    if (c.head_hidden > 0) p.head_hid = take(sizeof(float) * static_cast<size_t>(n) * c.head_hidden);
     p.total = o;
     return p;
 }
@@ -152,7 +159,7 @@ size_t elis_predict_workspace_bytes(const elis_config* cfg, int32_t total_tokens
     if (check_config(cfg) != ELIS_OK || n_seqs <= 0 || total_tokens < n_seqs || max_seqlen < 1 ||
         max_seqlen > cfg->max_pos)
         return 0;
-    return predict_layout(*cfg, total_tokens, n_seqs).total;
+    return predict_layout(*cfg, total_tokens, n_seqs, max_seqlen).total;
 }
 
 int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, const int32_t* cu_seqlens,
@@ -165,7 +172,7 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
     if (!aligned(workspace)) return ELIS_EINVAL;
     const elis_config& c = w->cfg;
     if (max_seqlen < 1 || max_seqlen > c.max_pos || total_tokens < n_seqs) return ELIS_ESHAPE;
-    const PredictLayout p = predict_layout(c, total_tokens, n_seqs);
+    const PredictLayout p = predict_layout(c, total_tokens, n_seqs, max_seqlen);
     if (ws_bytes < p.total) return ELIS_EWORKSPACE;
 
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -221,8 +228,11 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
         if (e != hipSuccess) return status_of(e);
     }
     e = timed(ELIS_K_POOL_HEAD, st, [&] {
+        const PoolScratch scr{c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_partial) : nullptr,
+                              c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_z) : nullptr,
+                              c.head_hidden > 0 ? at<float>(workspace, p.head_hid) : nullptr, p.nchunk};
         return launch_pool_head(final32, tab, n, d, c.pooling, c.head_hidden, w->head_w1, w->head_b1, w->head_w2,
-                                w->head_b2, c.out_scale, c.out_shift, out_pred, st);
+                                w->head_b2, c.out_scale, c.out_shift, out_pred, scr, st);
     });
     return status_of(e);
 }

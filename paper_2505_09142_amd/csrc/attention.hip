@@ -21,7 +21,9 @@
 //
 // LDS. K is stored row-major with 16-byte chunks XOR-swizzled by row; V is
 // stored transposed (V^T[d][key], rows padded to 72 keys) so that a lane's
-// 8 keys for one d are two 8-byte reads.
+// 8 keys for one d are two 8-byte reads. Two LDS buffers: the next tile is
+// fetched from HBM into registers while the current one is multiplied, so
+// each tile costs one barrier and its load latency is hidden.
 #include <math.h>
 
 #include "kernels.h"
@@ -54,8 +56,8 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     constexpr int CPR = DH / 8;   // 16-byte chunks per head row
     constexpr int KS = DH / 32;   // MFMA k-steps over d_head
     constexpr int DT = DH / 16;   // 16-wide d blocks of the output
-    __shared__ __attribute__((aligned(16))) uint16_t sK[kBKV * DH];
-    __shared__ __attribute__((aligned(16))) uint16_t sVt[DH * kVtStride];
+    __shared__ __attribute__((aligned(16))) uint16_t sK[2 * kBKV * DH];
+    __shared__ __attribute__((aligned(16))) uint16_t sVt[2 * DH * kVtStride];
 
     const int tile = blockIdx.x, h = blockIdx.y;
     if (tile >= tile_off[n]) return;  // uniform over the work-group
@@ -91,32 +93,76 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     float m_run[2] = {-INFINITY, -INFINITY};
     float l_run[2] = {0.f, 0.f};
 
-    for (int kv0 = 0; kv0 < L; kv0 += kBKV) {
-        // K tile -> LDS, row-major, swizzled chunks.
-        for (int c = tid; c < kBKV * CPR; c += kWaves * kWave) {
-            const int row = c / CPR, ch = c % CPR;
-            int tok = kv0 + row;
-            tok = tok < L ? tok : L - 1;
-            const u32x4 v = *reinterpret_cast<const u32x4*>(Kg + static_cast<size_t>(seq0 + tok) * D3 + ch * 8);
-            *reinterpret_cast<u32x4*>(&sK[row * DH + ((ch ^ kswz<DH>(row)) * 8)]) = v;
-        }
-        // V tile -> LDS transposed; a thread moves 2 keys x 8 d.
-        for (int u = tid; u < (kBKV / 2) * CPR; u += kWaves * kWave) {
-            const int tp = u % (kBKV / 2), ch = u / (kBKV / 2);
-            int t0 = kv0 + 2 * tp, t1 = t0 + 1;
-            t0 = t0 < L ? t0 : L - 1;
-            t1 = t1 < L ? t1 : L - 1;
-            const u32x4 a = *reinterpret_cast<const u32x4*>(Vg + static_cast<size_t>(seq0 + t0) * D3 + ch * 8);
-            const u32x4 b = *reinterpret_cast<const u32x4*>(Vg + static_cast<size_t>(seq0 + t1) * D3 + ch * 8);
+    // Staging of one 64-key tile: K as 16-byte row chunks, V as pairs of rows (2 keys x 8 d).
+    constexpr int KCH = kBKV * CPR;                 // K chunks per tile
+    constexpr int VCH = (kBKV / 2) * CPR;           // V units per tile
+    constexpr int KPT = (KCH + kWaves * kWave - 1) / (kWaves * kWave);
+    constexpr int VPT = (VCH + kWaves * kWave - 1) / (kWaves * kWave);
+    u32x4 rk[KPT], rv0[VPT], rv1[VPT];
+    auto gload = [&](int kv0) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t lo = (a[e] & 0xffffu) | (b[e] << 16);
-                const uint32_t hi = (a[e] >> 16) | (b[e] & 0xffff0000u);
-                *reinterpret_cast<uint32_t*>(&sVt[(ch * 8 + 2 * e) * kVtStride + 2 * tp]) = lo;
-                *reinterpret_cast<uint32_t*>(&sVt[(ch * 8 + 2 * e + 1) * kVtStride + 2 * tp]) = hi;
+        for (int i = 0; i < KPT; ++i) {
+            const int c = tid + i * kWaves * kWave;
+            if (KCH % (kWaves * kWave) == 0 || c < KCH) {
+                const int row = c / CPR, ch = c % CPR;
+                int tok = kv0 + row;
+                tok = tok < L ? tok : L - 1;
+                rk[i] = *reinterpret_cast<const u32x4*>(Kg + static_cast<size_t>(seq0 + tok) * D3 + ch * 8);
             }
         }
+#pragma unroll
+        for (int i = 0; i < VPT; ++i) {
+            const int u = tid + i * kWaves * kWave;
+            if (VCH % (kWaves * kWave) == 0 || u < VCH) {
+                const int tp = u % (kBKV / 2), ch = u / (kBKV / 2);
+                int t0 = kv0 + 2 * tp, t1 = t0 + 1;
+                t0 = t0 < L ? t0 : L - 1;
+                t1 = t1 < L ? t1 : L - 1;
+                rv0[i] = *reinterpret_cast<const u32x4*>(Vg + static_cast<size_t>(seq0 + t0) * D3 + ch * 8);
+                rv1[i] = *reinterpret_cast<const u32x4*>(Vg + static_cast<size_t>(seq0 + t1) * D3 + ch * 8);
+            }
+        }
+    };
+    auto sstore = [&](int b) {
+        uint16_t* k_s = sK + b * (kBKV * DH);
+        uint16_t* v_s = sVt + b * (DH * kVtStride);
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) {
+            const int c = tid + i * kWaves * kWave;
+            if (KCH % (kWaves * kWave) == 0 || c < KCH) {
+                const int row = c / CPR, ch = c % CPR;
+                *reinterpret_cast<u32x4*>(&k_s[row * DH + ((ch ^ kswz<DH>(row)) * 8)]) = rk[i];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < VPT; ++i) {
+            const int u = tid + i * kWaves * kWave;
+            if (VCH % (kWaves * kWave) == 0 || u < VCH) {
+                const int tp = u % (kBKV / 2), ch = u / (kBKV / 2);
+                const u32x4 a = rv0[i], bb = rv1[i];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t lo = (a[e] & 0xffffu) | (bb[e] << 16);
+                    const uint32_t hi = (a[e] >> 16) | (bb[e] & 0xffff0000u);
+                    *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e) * kVtStride + 2 * tp]) = lo;
+                    *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e + 1) * kVtStride + 2 * tp]) = hi;
+                }
+            }
+        }
+    };
+
+    const int ntiles = (L + kBKV - 1) / kBKV;
+    gload(0);
+    for (int t = 0; t < ntiles; ++t) {
+        const int kv0 = t * kBKV;
+        const int b = t & 1;
+        // Buffer b was last read in tile t-2; the barrier of tile t-1 ordered those reads
+        // before these writes.
+        sstore(b);
         __syncthreads();
+        if (t + 1 < ntiles) gload(kv0 + kBKV);  // in flight while this tile is multiplied
+        const uint16_t* k_s = sK + b * (kBKV * DH);
+        const uint16_t* v_s = sVt + b * (DH * kVtStride);
 
         // S^T = K Q^T: 4 key blocks x 2 query blocks.
         f32x4 sc[4][2];
@@ -127,14 +173,15 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 const int ch = ks * 4 + g;
-                kf[ks] = *reinterpret_cast<const bf16x8*>(&sK[row * DH + ((ch ^ kswz<DH>(row)) * 8)]);
+                kf[ks] = *reinterpret_cast<const bf16x8*>(&k_s[row * DH + ((ch ^ kswz<DH>(row)) * 8)]);
             }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
+                f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks], qf[j][ks], a, 0, 0, 0);
-                sc[tt][j] = a;
+                for (int ks = 0; ks < KS; ++ks)
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[ks], qf[j][ks], acc, 0, 0, 0);
+                sc[tt][j] = acc;
             }
         }
 
@@ -188,8 +235,8 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
             const int d = dt * 16 + r16;
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
-                const u32x2 lo = *reinterpret_cast<const u32x2*>(&sVt[d * kVtStride + kc * 32 + 4 * g]);
-                const u32x2 hi = *reinterpret_cast<const u32x2*>(&sVt[d * kVtStride + kc * 32 + 16 + 4 * g]);
+                const u32x2 lo = *reinterpret_cast<const u32x2*>(&v_s[d * kVtStride + kc * 32 + 4 * g]);
+                const u32x2 hi = *reinterpret_cast<const u32x2*>(&v_s[d * kVtStride + kc * 32 + 16 + 4 * g]);
                 u32x4 w;
                 w[0] = lo[0];
                 w[1] = lo[1];
@@ -197,10 +244,10 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                 w[3] = hi[1];
                 const bf16x8 vf = __builtin_bit_cast(bf16x8, w);
 #pragma unroll
-                for (int j = 0; j < 2; ++j) o[dt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc][j], o[dt][j], 0, 0, 0);
+                for (int j = 0; j < 2; ++j)
+                    o[dt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc][j], o[dt][j], 0, 0, 0);
             }
         }
-        __syncthreads();
     }
 
     // Normalise and store: lane holds O[query j*16 + r16][d = dt*16 + 4g .. +3].

@@ -25,6 +25,8 @@
 // to the 8 XCDs (each with its own L2). Ids are remapped so every XCD gets one
 // contiguous range of tiles, ordered N-fastest: the tiles an XCD runs together
 // share their activation rows, which are then fetched from HBM once per XCD.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace elis {
@@ -43,20 +45,65 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblk) {
     return xcd * per + (xcd < rem ? xcd : rem) + local;
 }
 
-__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+// GELU(x) = x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf from Abramowitz & Stegun 7.1.26:
+// for z >= 0, erfc(z) = (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2) + e(z),
+// t = 1 / (1 + p z), |e(z)| <= 1.5e-7. Branch-free: one reciprocal, one exp2, five FMAs.
+// LDS chunk swizzle of the direct-to-LDS kernels: physical 16-byte chunk = logical chunk ^ swz(row).
+// Measured free of bank conflicts on gfx950 for both 16-row and 32-row fragment reads (the
+// plain row & 7 form conflicts 4-way on 32-row reads).
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+__device__ __forceinline__ float gelu_erf(float x) {
+    constexpr float p = 0.3275911f;
+    constexpr float a1 = 0.254829592f, a2 = -0.284496736f, a3 = 1.421413741f, a4 = -1.453152027f,
+                    a5 = 1.061405429f;
+    const float z = fabsf(x) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(p, z, 1.0f));
+    const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, a5, a4), a3), a2), a1);
+    const float tail = poly * __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);  // erfc(|x|/sqrt 2)
+    return 0.5f * x * (x >= 0.f ? 2.0f - tail : tail);
+}
+
+// One MFMA block of the wave tile: MI x MI outputs (MI = 16: 16x16x32, MI = 32: 32x32x16).
+template <int MI>
+struct Mfma;
+
+template <>
+struct Mfma<16> {
+    typedef f32x4 acc_t;
+    static constexpr int kRegs = 4;
+    static constexpr int kDepth = 32;  // k per instruction
+    __device__ static __forceinline__ acc_t run(bf16x8 a, bf16x8 b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <>
+struct Mfma<32> {
+    typedef f32x16 acc_t;
+    static constexpr int kRegs = 16;
+    static constexpr int kDepth = 16;
+    __device__ static __forceinline__ acc_t run(bf16x8 a, bf16x8 b, acc_t c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <int BM, int BN, int WM, int WN, int MI, int EPI>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __restrict__ A,
                                                              const uint16_t* __restrict__ B,
                                                              const float* __restrict__ bias,
                                                              const float* __restrict__ res, void* __restrict__ out,
                                                              int M, int N, int K) {
+    typedef Mfma<MI> MF;
+    typedef typename MF::acc_t acc_t;
     constexpr int NT = WM * WN * kWave;
     constexpr int TM = BM / WM, TN = BN / WN;
-    constexpr int FM = TM / 16, FN = TN / 16;
+    constexpr int FM = TM / MI, FN = TN / MI;
+    constexpr int KSTEPS = kBK / MF::kDepth;
+    constexpr int GROUPS = kWave / MI;  // lane groups along k (4 for MI 16, 2 for MI 32)
     constexpr int ACH = BM * 8 / NT, BCH = BN * 8 / NT;  // 16-byte chunks per thread per k-slab
     static_assert(BM * 8 % NT == 0 && BN * 8 % NT == 0, "tile must split evenly over the threads");
-    static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile must be a multiple of 16");
+    static_assert(TM % MI == 0 && TN % MI == 0, "wave tile must be a multiple of the MFMA block");
 
     __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * kBK];
     __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * kBK];
@@ -88,11 +135,13 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __r
     }
 
     u32x4 ra[ACH], rb[BCH];
-    f32x4 acc[FM][FN];
+    acc_t acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::kRegs; ++r) acc[i][j][r] = 0.f;
 
     auto gload = [&](int k0) {
 #pragma unroll
@@ -112,81 +161,537 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __r
     sstore(0);
     __syncthreads();
 
-    const int r16 = lane & 15, kg = lane >> 4;
+    const int rl = lane % MI, kg = lane / MI;
     for (int kt = 0; kt < KT; ++kt) {
         const int cur = kt & 1;
         if (kt + 1 < KT) gload((kt + 1) * kBK);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int c = ks * 4 + kg;
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            const int c = ks * GROUPS + kg;  // 16-byte chunk (8 k values) this lane feeds
             bf16x8 af[FM], bfr[FN];
 #pragma unroll
             for (int i = 0; i < FM; ++i) {
-                const int row = wm * TM + i * 16 + r16;
+                const int row = wm * TM + i * MI + rl;
                 af[i] = *reinterpret_cast<const bf16x8*>(&sA[cur][row * kBK + ((c ^ (row & 7)) * 8)]);
             }
 #pragma unroll
             for (int j = 0; j < FN; ++j) {
-                const int row = wn * TN + j * 16 + r16;
+                const int row = wn * TN + j * MI + rl;
                 bfr[j] = *reinterpret_cast<const bf16x8*>(&sB[cur][row * kBK + ((c ^ (row & 7)) * 8)]);
             }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < FN; ++j) acc[i][j] = MF::run(bfr[j], af[i], acc[i][j]);
         }
         if (kt + 1 < KT) sstore(cur ^ 1);
         __syncthreads();
     }
 
-    // Epilogue: lane holds C[m][n .. n+3] for m = row r16 of block i, n = 4*kg in block j.
+    // Epilogue. Lane holds, for output row m = rl of block i, groups of 4 consecutive
+    // columns: MI 16: one group at 4*kg; MI 32: four groups at 8*q + 4*kg.
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-        const int m = m0 + wm * TM + i * 16 + r16;
+        const int m = m0 + wm * TM + i * MI + rl;
         if (m >= M) continue;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-            const int n = n0 + wn * TN + j * 16 + 4 * kg;
-            f32x4 v = acc[i][j] + *reinterpret_cast<const f32x4*>(bias + n);
-            const size_t o = static_cast<size_t>(m) * N + n;
-            if constexpr (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2) {
-                v += *reinterpret_cast<const f32x4*>(res + o);
-                *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
-            } else {
-                if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) v[c] = gelu_erf(v[c]);
+            for (int q = 0; q < MF::kRegs / 4; ++q) {
+                const int n = n0 + wn * TN + j * MI + 8 * q + 4 * kg;
+                f32x4 v;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+                v += *reinterpret_cast<const f32x4*>(bias + n);
+                const size_t o = static_cast<size_t>(m) * N + n;
+                if constexpr (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2) {
+                    v += *reinterpret_cast<const f32x4*>(res + o);
+                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
+                } else {
+                    if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) v[c] = gelu_erf(v[c]);
+                    }
+                    u32x2 p;
+                    p[0] = pack_bf16x2(v[0], v[1]);
+                    p[1] = pack_bf16x2(v[2], v[3]);
+                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + o) = p;
                 }
-                u32x2 p;
-                p[0] = pack_bf16x2(v[0], v[1]);
-                p[1] = pack_bf16x2(v[2], v[3]);
-                *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + o) = p;
             }
         }
     }
 }
 
-template <int BM, int BN, int WM, int WN>
+// ---------------------------------------------------------------------------------------------
+// Multi-stage variant: k-slabs go from HBM straight into LDS (global_load_lds_dwordx4, no
+// register staging), S stages deep, so S-1 slabs are in flight while one is multiplied.
+// Each thread waits (vmcnt) only for its own loads of the slab about to be consumed; the
+// barrier that follows makes every thread's part of that slab visible and also guarantees
+// that every wave has finished reading the stage the next loads will overwrite.
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    // gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14; expcnt/lgkmcnt left at max.
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// One wave-wide 16-byte-per-lane load from global memory straight into LDS: lane i's 16 bytes
+// land at lds + 16 * i.
+__device__ __forceinline__ void load_lds_16(const void* src, void* lds) {
+    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)lds, 16, 0, 0);
+}
+
+__device__ __forceinline__ void block_sync_lds() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Tile index -> (tile row, tile col), grouping GM tile rows so that the tiles running
+// together on one XCD share a small set of A rows and B columns (L2 reuse).
+__device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, int gm, int& tm, int& tn) {
+    const int per_group = gm * tiles_n;
+    const int g = t / per_group, first = g * gm;
+    const int rows = (tiles_m - first) < gm ? (tiles_m - first) : gm;
+    const int r = t - g * per_group;
+    tm = first + r % rows;
+    tn = r / rows;
+}
+
+template <int BM, int BN, int WM, int WN, int MI, int S, int EPI>
+__global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t* __restrict__ A,
+                                                                  const uint16_t* __restrict__ B,
+                                                                  const float* __restrict__ bias,
+                                                                  const float* __restrict__ res,
+                                                                  void* __restrict__ out, int M, int N, int K,
+                                                                  int group_m) {
+    typedef Mfma<MI> MF;
+    typedef typename MF::acc_t acc_t;
+    constexpr int NW = WM * WN;
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int FM = TM / MI, FN = TN / MI;
+    constexpr int KSTEPS = kBK / MF::kDepth;
+    constexpr int GROUPS = kWave / MI;
+    constexpr int RPI = kWave * 16 / (kBK * 2);   // rows covered by one wave-wide 16-byte load: 8
+    constexpr int LA = BM / RPI / NW, LB = BN / RPI / NW;  // loads per wave per stage
+    constexpr int STAGE = (BM + BN) * kBK;       // bf16 elements per stage
+    static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "rows must split over the waves");
+    static_assert(S >= 2 && (S - 1) * (LA + LB) < 64, "pipeline depth");
+
+    __shared__ __attribute__((aligned(1024))) uint16_t smem[S * STAGE];
+
+    const int tiles_n = N / BN;
+    const int tiles_m = (M + BM - 1) / BM;
+    int tm, tn;
+    grouped_tile(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, group_m, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int wm = wid / WN, wn = wid % WN;
+
+    // Global source of this lane for each of its loads: LDS row = base + lane / 8, physical
+    // chunk lane % 8, which holds logical chunk (lane % 8) ^ (row & 7).
+    const uint16_t* ga[LA];
+    const uint16_t* gb[LB];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+        const int row = (wid * LA + i) * RPI + lane / 8;
+        const int c = (lane & 7) ^ swz(row);
+        const int gr = (m0 + row < M) ? m0 + row : M - 1;
+        ga[i] = A + static_cast<size_t>(gr) * K + c * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+        const int row = (wid * LB + i) * RPI + lane / 8;
+        const int c = (lane & 7) ^ swz(row);
+        gb[i] = B + static_cast<size_t>(n0 + row) * K + c * 8;
+    }
+
+    auto issue = [&](int kt) {
+        uint16_t* st = smem + (kt % S) * STAGE;
+        const int k0 = kt * kBK;
+#pragma unroll
+        for (int i = 0; i < LA; ++i)
+            load_lds_16(ga[i] + k0, st + (wid * LA + i) * RPI * kBK);
+#pragma unroll
+        for (int i = 0; i < LB; ++i)
+            load_lds_16(gb[i] + k0, st + BM * kBK + (wid * LB + i) * RPI * kBK);
+    };
+
+    acc_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::kRegs; ++r) acc[i][j][r] = 0.f;
+
+    const int KT = K / kBK;
+#pragma unroll
+    for (int p = 0; p < S - 1; ++p)
+        if (p < KT) issue(p);
+
+    const int rl = lane % MI, kg = lane / MI;
+    for (int kt = 0; kt < KT; ++kt) {
+        // loads issued after slab kt: min(S-2, KT-1-kt) stages
+        const int later = (KT - 1 - kt) < (S - 2) ? (KT - 1 - kt) : (S - 2);
+        if constexpr (S >= 4) {
+            if (later >= 2) wait_vmcnt<2 * (LA + LB)>();
+            else if (later == 1) wait_vmcnt<(LA + LB)>();
+            else wait_vmcnt<0>();
+        } else if constexpr (S == 3) {
+            if (later >= 1) wait_vmcnt<(LA + LB)>();
+            else wait_vmcnt<0>();
+        } else {
+            wait_vmcnt<0>();
+        }
+        block_sync_lds();
+        if (kt + S - 1 < KT) issue(kt + S - 1);
+        const uint16_t* sA = smem + (kt % S) * STAGE;
+        const uint16_t* sB = sA + BM * kBK;
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            const int c = ks * GROUPS + kg;
+            bf16x8 af[FM], bfr[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int row = wm * TM + i * MI + rl;
+                af[i] = *reinterpret_cast<const bf16x8*>(&sA[row * kBK + ((c ^ swz(row)) * 8)]);
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int row = wn * TN + j * MI + rl;
+                bfr[j] = *reinterpret_cast<const bf16x8*>(&sB[row * kBK + ((c ^ swz(row)) * 8)]);
+            }
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) acc[i][j] = MF::run(bfr[j], af[i], acc[i][j]);
+        }
+    }
+
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int m = m0 + wm * TM + i * MI + rl;
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+#pragma unroll
+            for (int q = 0; q < MF::kRegs / 4; ++q) {
+                const int n = n0 + wn * TN + j * MI + 8 * q + 4 * kg;
+                f32x4 v;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+                v += *reinterpret_cast<const f32x4*>(bias + n);
+                const size_t o = static_cast<size_t>(m) * N + n;
+                if constexpr (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2) {
+                    v += *reinterpret_cast<const f32x4*>(res + o);
+                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
+                } else {
+                    if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) v[c] = gelu_erf(v[c]);
+                    }
+                    u32x2 p;
+                    p[0] = pack_bf16x2(v[0], v[1]);
+                    p[1] = pack_bf16x2(v[2], v[3]);
+                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + o) = p;
+                }
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int WM, int WN, int MI, int S>
+hipError_t launch_dlds(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
+                       int k, int epi, void* out, hipStream_t st, int group_m) {
+    const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
+    switch (epi) {
+        case ELIS_EPI_BIAS_BF16:
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x,
+                               w, bias, res, out, m, n, k, group_m);
+            break;
+        case ELIS_EPI_BIAS_GELU_BF16:
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0,
+                               st, x, w, bias, res, out, m, n, k, group_m);
+            break;
+        case ELIS_EPI_BIAS_RES_F32:
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st,
+                               x, w, bias, res, out, m, n, k, group_m);
+            break;
+        case kEpiResF32Ffn2:
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResF32Ffn2>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k, group_m);
+            break;
+        default:
+            return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------------
+// Scheduled variant: 4 waves (2 x 2), each owning a (BM/2) x (BN/2) block of MFMA tiles; two
+// LDS stages filled by direct-to-LDS loads. A 64-deep k-slab is consumed in k-steps whose
+// operand fragments are double-buffered in registers, so the LDS reads of the next k-step
+// run under the MFMAs of the current one. The slab two steps ahead is requested right after
+// the barrier that frees its stage (before the last k-step of the current slab), so a load
+// has one full slab of MFMA work to arrive. sched_group_barrier spreads the LDS reads and the
+// direct loads evenly between the MFMAs.
+//
+// LDS chunk swizzle: physical chunk = logical chunk ^ ((row >> 1) & 7). Measured free of bank
+// conflicts on gfx950 for both the 16-row (16x16x32) and 32-row (32x32x16) fragment reads;
+// the plain (row & 7) form conflicts 4-way on the 32-row reads.
+
+template <int N>
+__device__ __forceinline__ void wait_lgkm() {
+    __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (N << 8) | (3 << 14));
+}
+
+// NM MFMA groups, with NV direct loads and ND LDS reads spread evenly in front of them.
+template <int G, int NM, int NV, int ND, int SYNC>
+__device__ __forceinline__ void interleave_step() {
+    if constexpr (G < NM) {
+        constexpr int v = (G + 1) * NV / NM - G * NV / NM;
+        constexpr int d = (G + 1) * ND / NM - G * ND / NM;
+        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, SYNC);
+        if constexpr (d > 0) __builtin_amdgcn_sched_group_barrier(0x100, d, SYNC);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, SYNC);
+        interleave_step<G + 1, NM, NV, ND, SYNC>();
+    }
+}
+
+template <int BM, int BN, int MI, int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_sched_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, const float* __restrict__ bias,
+    const float* __restrict__ res, void* __restrict__ out, int M, int N, int K, int group_m) {
+    typedef Mfma<MI> MF;
+    typedef typename MF::acc_t acc_t;
+    constexpr int TM = BM / 2, TN = BN / 2;
+    constexpr int FM = TM / MI, FN = TN / MI;
+    constexpr int KS = kBK / MF::kDepth;   // k-steps per slab (2 for 16x16x32, 4 for 32x32x16)
+    constexpr int GROUPS = kWave / MI;     // lane groups along k
+    constexpr int LA = BM / 8 / 4, LB = BN / 8 / 4;  // direct loads per wave per stage
+    constexpr int STAGE = (BM + BN) * kBK;
+    constexpr int NMF = FM * FN, NRD = FM + FN, NGL = LA + LB;
+    static_assert(KS % 2 == 0, "fragment buffers alternate per k-step");
+    __shared__ __attribute__((aligned(1024))) uint16_t smem[2 * STAGE];
+
+    const int tiles_n = N / BN;
+    const int tiles_m = (M + BM - 1) / BM;
+    int tm, tn;
+    grouped_tile(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, group_m, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int wm = wid >> 1, wn = wid & 1;
+
+    const uint16_t* ga[LA];
+    const uint16_t* gb[LB];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+        const int row = (wid * LA + i) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ swz(row);
+        const int gr = (m0 + row < M) ? m0 + row : M - 1;
+        ga[i] = A + static_cast<size_t>(gr) * K + c * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+        const int row = (wid * LB + i) * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ swz(row);
+        gb[i] = B + static_cast<size_t>(n0 + row) * K + c * 8;
+    }
+    auto issue = [&](int kt) {
+        uint16_t* st = smem + (kt & 1) * STAGE;
+        const int k0 = kt * kBK;
+#pragma unroll
+        for (int i = 0; i < LA; ++i) load_lds_16(ga[i] + k0, st + (wid * LA + i) * 8 * kBK);
+#pragma unroll
+        for (int i = 0; i < LB; ++i) load_lds_16(gb[i] + k0, st + BM * kBK + (wid * LB + i) * 8 * kBK);
+    };
+
+    const int rl = lane % MI, kg = lane / MI;
+    int offa[FM], offb[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) offa[i] = (wm * TM + i * MI + rl) * kBK;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) offb[j] = BM * kBK + (wn * TN + j * MI + rl) * kBK;
+    const int rs = swz(rl);  // fragment rows start at multiples of 16, so swz(row) == swz(rl)
+
+    bf16x8 fa[2][FM], fb[2][FN];
+    auto load_frags = [&](int buf, int stage, int ks) {
+        const uint16_t* st = smem + stage * STAGE;
+        const int c = ((ks * GROUPS + kg) ^ rs) * 8;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[i] + c);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[j] + c);
+    };
+
+    acc_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::kRegs; ++r) acc[i][j][r] = 0.f;
+
+    auto mfma_all = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = MF::run(fb[buf][j], fa[buf][i], acc[i][j]);
+    };
+
+    const int KT = K / kBK;
+    issue(0);
+    if (KT > 1) {
+        issue(1);
+        wait_vmcnt<NGL>();
+    } else {
+        wait_vmcnt<0>();
+    }
+    block_sync_lds();
+    load_frags(0, 0, 0);
+
+    // One slab. ISSUE: request slab kt+2; NEXT: slab kt+1 exists (read its first fragments).
+    // Both are compile-time so the steady-state loop is straight-line code.
+    auto slab = [&](int kt, auto issue_c, auto next_c) {
+        constexpr bool ISSUE = decltype(issue_c)::value, NEXT = decltype(next_c)::value;
+        const int cur = kt & 1;
+#pragma unroll
+        for (int ks = 0; ks < KS - 1; ++ks) {
+            load_frags((ks + 1) & 1, cur, ks + 1);
+            mfma_all(ks & 1);
+            interleave_step<0, NMF, 0, NRD, 0>();
+        }
+        // Slab kt+1 has landed and every wave's reads of stage `cur` are complete.
+        wait_vmcnt<0>();
+        wait_lgkm<0>();
+        block_sync_lds();
+        if constexpr (ISSUE) issue(kt + 2);
+        if constexpr (NEXT) load_frags(0, cur ^ 1, 0);
+        mfma_all((KS - 1) & 1);
+        interleave_step<0, NMF, ISSUE ? NGL : 0, NEXT ? NRD : 0, 1>();
+    };
+    typedef std::integral_constant<bool, true> T_;
+    typedef std::integral_constant<bool, false> F_;
+    int kt = 0;
+    for (; kt + 2 < KT; ++kt) slab(kt, T_(), T_());
+    if (kt + 1 < KT) slab(kt++, F_(), T_());
+    slab(kt, F_(), F_());
+
+    // Epilogue through LDS: each wave stages one 32-row block row of its output tile (bias,
+    // activation / residual applied), then writes it back as whole rows, 16 bytes per lane,
+    // so every store instruction covers full cache lines.
+    static_assert(MI == 32, "staged epilogue assumes 32-row MFMA blocks");
+    constexpr bool F32OUT = (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2);
+    constexpr int EB = F32OUT ? 4 : 2;          // output element bytes
+    constexpr int ROWB = TN * EB;               // bytes of one wave-tile row
+    constexpr int PITCH = ROWB + 16;            // padded LDS row pitch
+    constexpr int LPR = ROWB / 16;              // lanes per row on read-back
+    constexpr int RPI = kWave / LPR;            // rows per read-back instruction
+    static_assert(4 * 32 * PITCH <= 2 * STAGE * 2, "staging must fit in the stage buffers");
+    block_sync_lds();  // every wave is done with the stage buffers
+    char* stg = reinterpret_cast<char*>(smem) + wid * 32 * PITCH;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = j * MI + 8 * q + 4 * kg;
+                f32x4 v;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+                v += *reinterpret_cast<const f32x4*>(bias + n0 + wn * TN + col);
+                if constexpr (F32OUT) {
+                    *reinterpret_cast<f32x4*>(stg + rl * PITCH + col * 4) = v;
+                } else {
+                    if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) v[c] = gelu_erf(v[c]);
+                    }
+                    u32x2 pk;
+                    pk[0] = pack_bf16x2(v[0], v[1]);
+                    pk[1] = pack_bf16x2(v[2], v[3]);
+                    *reinterpret_cast<u32x2*>(stg + rl * PITCH + col * 2) = pk;
+                }
+            }
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_wave_barrier();
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int rr = 0; rr < 32 / RPI; ++rr) {
+            const int row = rr * RPI + lane / LPR, ch = lane % LPR;
+            const int m = m0 + wm * TM + i * MI + row;
+            const u32x4 d = *reinterpret_cast<const u32x4*>(stg + row * PITCH + ch * 16);
+            if (m < M) {
+                const size_t o = static_cast<size_t>(m) * N + n0 + wn * TN + ch * (16 / EB);
+                if constexpr (F32OUT) {
+                    f32x4 v = __builtin_bit_cast(f32x4, d) + *reinterpret_cast<const f32x4*>(res + o);
+                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
+                } else {
+                    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(out) + o) = d;
+                }
+            }
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_wave_barrier();
+        asm volatile("" ::: "memory");
+    }
+}
+
+template <int BM, int BN, int MI>
+hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
+                        int k, int epi, void* out, hipStream_t st, int group_m) {
+    const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(256);
+    switch (epi) {
+        case ELIS_EPI_BIAS_BF16:
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w, bias,
+                               res, out, m, n, k, group_m);
+            break;
+        case ELIS_EPI_BIAS_GELU_BF16:
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k, group_m);
+            break;
+        case ELIS_EPI_BIAS_RES_F32:
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k, group_m);
+            break;
+        case kEpiResF32Ffn2:
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, kEpiResF32Ffn2>), grid, block, 0, st, x, w, bias, res,
+                               out, m, n, k, group_m);
+            break;
+        default:
+            return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int MI>
 hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
                        int k, int epi, void* out, hipStream_t st) {
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w, bias,
-                               res, out, m, n, k);
-            break;
-        case ELIS_EPI_BIAS_GELU_BF16:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x, w,
+            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k);
             break;
+        case ELIS_EPI_BIAS_GELU_BF16:
+            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x,
+                               w, bias, res, out, m, n, k);
+            break;
         case ELIS_EPI_BIAS_RES_F32:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
+            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k);
             break;
         case kEpiResF32Ffn2:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, kEpiResF32Ffn2>), grid, block, 0, st, x, w, bias, res,
-                               out, m, n, k);
+            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, kEpiResF32Ffn2>), grid, block, 0, st, x, w, bias,
+                               res, out, m, n, k);
             break;
         default:
             return hipErrorInvalidValue;
@@ -196,12 +701,43 @@ hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, 
 
 }  // namespace
 
+// Tile configurations (ids are internal; benchmarks sweep them).
+hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uint16_t* w, const float* bias,
+                              const float* res, int m, int n, int k, int epi, void* out, hipStream_t st) {
+    switch (cfg) {
+        case 0: return launch_tile<128, 128, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
+        case 1: return launch_tile<128, 64, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
+        case 14: return launch_dlds<256, 256, 2, 4, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 19: return launch_dlds<128, 128, 2, 2, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 20: return launch_sched<256, 256, 32>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+int gemm_config_bn(int cfg) {
+    switch (cfg) {
+        case 1: return 64;
+        case 14: case 20: return 256;
+        default: return 128;
+    }
+}
+
+// Per-shape choice, from measurements on MI355X over the encoder's GEMM shapes
+// (M = 24K..110K tokens; (N, K) = (3d, d), (d, d), (F, d), (d, F)):
+//   bf16 out, bias only (QKV):      scheduled 256 x 256, 32x32x16 MFMA, staged epilogue
+//   bf16 out, bias + GELU (FFN1):   8-wave 256 x 256 direct-to-LDS
+//   fp32 out, bias + residual:      4-wave 128 x 128 direct-to-LDS (more tiles in flight,
+//                                   better for the HBM-heavy fp32 epilogue)
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
                        int k, int epi, void* out, hipStream_t st, bool ffn2) {
     if (ffn2 && epi == ELIS_EPI_BIAS_RES_F32) epi = kEpiResF32Ffn2;
     if (m < 1 || n % 64 != 0 || k % kBK != 0 || n < 64 || k < kBK) return hipErrorInvalidValue;
-    if (n % 128 == 0) return launch_tile<128, 128, 2, 2>(x, w, bias, res, m, n, k, epi, out, st);
-    return launch_tile<128, 64, 2, 2>(x, w, bias, res, m, n, k, epi, out, st);
+    constexpr int kGroupM = 8;
+    if (n % 256 == 0 && epi == ELIS_EPI_BIAS_BF16) return launch_gemm_config(20, kGroupM, x, w, bias, res, m, n, k, epi, out, st);
+    if (n % 256 == 0 && epi == ELIS_EPI_BIAS_GELU_BF16)
+        return launch_gemm_config(14, kGroupM, x, w, bias, res, m, n, k, epi, out, st);
+    if (n % 128 == 0) return launch_gemm_config(19, kGroupM, x, w, bias, res, m, n, k, epi, out, st);
+    return launch_gemm_config(1, 1, x, w, bias, res, m, n, k, epi, out, st);
 }
 
 }  // namespace elis

@@ -23,14 +23,25 @@ hipError_t launch_layernorm(const float* x, const float* g, const float* b, int 
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m,
                        int n, int k, int epi, void* out, hipStream_t st, bool ffn2 = false);
 
+hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uint16_t* w, const float* bias,
+                              const float* res, int m, int n, int k, int epi, void* out, hipStream_t st);
+int gemm_config_bn(int cfg);
+
 // attention.hip
 hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh,
                             uint16_t* out, hipStream_t st);
 
 // pool_head.hip
+constexpr int kPoolChunk = 64;  // rows per partial sum of mean pooling
+struct PoolScratch {
+    float* partial;  // [n, nchunk, d]   (mean pooling)
+    float* z;        // [n, d]           (mean pooling)
+    float* hid;      // [n, head_hidden] (MLP head)
+    int nchunk;      // ceil(max_seqlen / kPoolChunk)
+};
 hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int pooling, int head_hidden,
                             const float* w1, const float* b1, const float* w2, const float* b2,
-                            float scale, float shift, float* out, hipStream_t st);
+                            float scale, float shift, float* out, PoolScratch scr, hipStream_t st);
 
 // select.hip
 int select_max_n();

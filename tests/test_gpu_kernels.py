@@ -103,7 +103,7 @@ def test_layernorm(rows, d):
 # ------------------------------------------------------------------------------ GEMM
 
 GEMM_CASES = [(1, 64, 64), (37, 128, 64), (300, 384, 128), (1000, 768, 768), (129, 3072, 768),
-              (517, 768, 3072), (2048, 2304, 768), (77, 192, 256)]
+              (517, 768, 3072), (2048, 2304, 768), (77, 192, 256), (64, 256, 64), (300, 512, 128), (1111, 1024, 4096)]
 
 
 @pytest.mark.parametrize("epi", [E.ELIS_EPI_BIAS_BF16, E.ELIS_EPI_BIAS_GELU_BF16, E.ELIS_EPI_BIAS_RES_F32])
