@@ -142,8 +142,9 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                 const u32x4 a = rv0[i], bb = rv1[i];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const uint32_t lo = (a[e] & 0xffffu) | (bb[e] << 16);
-                    const uint32_t hi = (a[e] >> 16) | (bb[e] & 0xffff0000u);
+                    // (key 2tp, key 2tp+1) pairs for d = 8ch+2e and 8ch+2e+1
+                    const uint32_t lo = __builtin_amdgcn_perm(bb[e], a[e], 0x05040100u);
+                    const uint32_t hi = __builtin_amdgcn_perm(bb[e], a[e], 0x07060302u);
                     *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e) * kVtStride + 2 * tp]) = lo;
                     *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e + 1) * kVtStride + 2 * tp]) = hi;
                 }
@@ -164,7 +165,9 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
         const uint16_t* k_s = sK + b * (kBKV * DH);
         const uint16_t* v_s = sVt + b * (DH * kVtStride);
 
-        // S^T = K Q^T: 4 key blocks x 2 query blocks.
+        if (qw >= L) continue;  // this wave's queries are all past the end (uniform per wave)
+
+        // S^T = K Q^T: 4 key blocks x 2 query blocks (raw scores, unscaled).
         f32x4 sc[4][2];
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt) {
@@ -184,48 +187,59 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                 sc[tt][j] = acc;
             }
         }
+        if (kv0 + kBKV > L) {  // last tile only: keys past the end get -inf (uniform branch)
+            const int valid = L - kv0;
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (tt * 16 + 4 * g + r >= valid) {
+                        sc[tt][0][r] = -INFINITY;
+                        sc[tt][1][r] = -INFINITY;
+                    }
+        }
 
-        // Online softmax (base 2; scale_log2 = log2(e) / sqrt(d_head)); keys past the end are masked.
-        const int valid = L - kv0;
+        // Online softmax. The running maximum is kept in raw-score units; the scale
+        // log2(e)/sqrt(d_head) enters once per score through the FMA inside exp2.
         bf16x8 pf[2][2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            float mx = -INFINITY;
+            float mx = fmaxf(fmaxf(sc[0][j][0], sc[0][j][1]), fmaxf(sc[0][j][2], sc[0][j][3]));
 #pragma unroll
-            for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int key = tt * 16 + 4 * g + r;
-                    const float x = key < valid ? sc[tt][j][r] * scale_log2 : -INFINITY;
-                    sc[tt][j][r] = x;
-                    mx = fmaxf(mx, x);
-                }
+            for (int tt = 1; tt < 4; ++tt)
+                mx = fmaxf(mx, fmaxf(fmaxf(sc[tt][j][0], sc[tt][j][1]), fmaxf(sc[tt][j][2], sc[tt][j][3])));
             mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
             mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
             const float m_new = fmaxf(m_run[j], mx);
-            const float alpha = exp2f(m_run[j] - m_new);
+            // alpha < 1 only where this tile raised the running maximum; once the maximum
+            // has settled (the common case after the first tiles) the whole wave skips the
+            // rescale of its output accumulators.
+            const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_new) * scale_log2);
+            const bool rescale = __builtin_amdgcn_ballot_w64(m_new != m_run[j]) != 0;
             m_run[j] = m_new;
-            float rs = 0.f;
+            const float nb = -m_new * scale_log2;
             float p[4][4];
+            float rs = 0.f;
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    p[tt][r] = exp2f(sc[tt][j][r] - m_new);
+                    p[tt][r] = __builtin_amdgcn_exp2f(fmaf(sc[tt][j][r], scale_log2, nb));
                     rs += p[tt][r];
                 }
-            l_run[j] = l_run[j] * alpha + rs;
+            l_run[j] = fmaf(l_run[j], alpha, rs);
+            if (rescale) {
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) o[dt][j] *= alpha;
+                for (int dt = 0; dt < DT; ++dt) o[dt][j] *= alpha;
+            }
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
-                bf16x8 f;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    f[r] = static_cast<__bf16>(p[2 * kc][r]);
-                    f[4 + r] = static_cast<__bf16>(p[2 * kc + 1][r]);
-                }
-                pf[kc][j] = f;
+                u32x4 w;
+                w[0] = pack_bf16x2(p[2 * kc][0], p[2 * kc][1]);
+                w[1] = pack_bf16x2(p[2 * kc][2], p[2 * kc][3]);
+                w[2] = pack_bf16x2(p[2 * kc + 1][0], p[2 * kc + 1][1]);
+                w[3] = pack_bf16x2(p[2 * kc + 1][2], p[2 * kc + 1][3]);
+                pf[kc][j] = __builtin_bit_cast(bf16x8, w);
             }
         }
 
