@@ -261,7 +261,7 @@ __device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, in
     tn = r / rows;
 }
 
-template <int BM, int BN, int WM, int WN, int MI, int S, int EPI>
+template <int BM, int BN, int WM, int WN, int MI, int S, int EPI, int BK = 64>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t* __restrict__ A,
                                                                   const uint16_t* __restrict__ B,
                                                                   const float* __restrict__ bias,
@@ -273,11 +273,13 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
     constexpr int NW = WM * WN;
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / MI, FN = TN / MI;
-    constexpr int KSTEPS = kBK / MF::kDepth;
+    constexpr int KSTEPS = BK / MF::kDepth;
     constexpr int GROUPS = kWave / MI;
-    constexpr int RPI = kWave * 16 / (kBK * 2);   // rows covered by one wave-wide 16-byte load: 8
+    constexpr int CPR = BK / 8;                  // 16-byte chunks per k-slab row
+    constexpr int RPI = kWave * 16 / (BK * 2);   // rows covered by one wave-wide 16-byte load
+    constexpr int SWS = BK == 64 ? 1 : 2;        // swizzle: chunk ^ ((row >> SWS) & (CPR - 1))
     constexpr int LA = BM / RPI / NW, LB = BN / RPI / NW;  // loads per wave per stage
-    constexpr int STAGE = (BM + BN) * kBK;       // bf16 elements per stage
+    constexpr int STAGE = (BM + BN) * BK;        // bf16 elements per stage
     static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "rows must split over the waves");
     static_assert(S >= 2 && (S - 1) * (LA + LB) < 64, "pipeline depth");
 
@@ -292,33 +294,33 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     const int wm = wid / WN, wn = wid % WN;
 
-    // Global source of this lane for each of its loads: LDS row = base + lane / 8, physical
-    // chunk lane % 8, which holds logical chunk (lane % 8) ^ (row & 7).
+    // Global source of this lane for each of its loads: LDS row = base + lane / CPR, physical
+    // chunk lane % CPR, which holds logical chunk (lane % CPR) ^ ((row >> SWS) & (CPR - 1)).
     const uint16_t* ga[LA];
     const uint16_t* gb[LB];
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
-        const int row = (wid * LA + i) * RPI + lane / 8;
-        const int c = (lane & 7) ^ swz(row);
+        const int row = (wid * LA + i) * RPI + lane / CPR;
+        const int c = (lane % CPR) ^ ((row >> SWS) & (CPR - 1));
         const int gr = (m0 + row < M) ? m0 + row : M - 1;
         ga[i] = A + static_cast<size_t>(gr) * K + c * 8;
     }
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
-        const int row = (wid * LB + i) * RPI + lane / 8;
-        const int c = (lane & 7) ^ swz(row);
+        const int row = (wid * LB + i) * RPI + lane / CPR;
+        const int c = (lane % CPR) ^ ((row >> SWS) & (CPR - 1));
         gb[i] = B + static_cast<size_t>(n0 + row) * K + c * 8;
     }
 
     auto issue = [&](int kt) {
         uint16_t* st = smem + (kt % S) * STAGE;
-        const int k0 = kt * kBK;
+        const int k0 = kt * BK;
 #pragma unroll
         for (int i = 0; i < LA; ++i)
-            load_lds_16(ga[i] + k0, st + (wid * LA + i) * RPI * kBK);
+            load_lds_16(ga[i] + k0, st + (wid * LA + i) * RPI * BK);
 #pragma unroll
         for (int i = 0; i < LB; ++i)
-            load_lds_16(gb[i] + k0, st + BM * kBK + (wid * LB + i) * RPI * kBK);
+            load_lds_16(gb[i] + k0, st + BM * BK + (wid * LB + i) * RPI * BK);
     };
 
     acc_t acc[FM][FN];
@@ -329,7 +331,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
 #pragma unroll
             for (int r = 0; r < MF::kRegs; ++r) acc[i][j][r] = 0.f;
 
-    const int KT = K / kBK;
+    const int KT = K / BK;
 #pragma unroll
     for (int p = 0; p < S - 1; ++p)
         if (p < KT) issue(p);
@@ -351,7 +353,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
         block_sync_lds();
         if (kt + S - 1 < KT) issue(kt + S - 1);
         const uint16_t* sA = smem + (kt % S) * STAGE;
-        const uint16_t* sB = sA + BM * kBK;
+        const uint16_t* sB = sA + BM * BK;
 #pragma unroll
         for (int ks = 0; ks < KSTEPS; ++ks) {
             const int c = ks * GROUPS + kg;
@@ -359,12 +361,12 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
 #pragma unroll
             for (int i = 0; i < FM; ++i) {
                 const int row = wm * TM + i * MI + rl;
-                af[i] = *reinterpret_cast<const bf16x8*>(&sA[row * kBK + ((c ^ swz(row)) * 8)]);
+                af[i] = *reinterpret_cast<const bf16x8*>(&sA[row * BK + ((c ^ ((row >> SWS) & (CPR - 1))) * 8)]);
             }
 #pragma unroll
             for (int j = 0; j < FN; ++j) {
                 const int row = wn * TN + j * MI + rl;
-                bfr[j] = *reinterpret_cast<const bf16x8*>(&sB[row * kBK + ((c ^ swz(row)) * 8)]);
+                bfr[j] = *reinterpret_cast<const bf16x8*>(&sB[row * BK + ((c ^ ((row >> SWS) & (CPR - 1))) * 8)]);
             }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
@@ -405,25 +407,25 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
     }
 }
 
-template <int BM, int BN, int WM, int WN, int MI, int S>
+template <int BM, int BN, int WM, int WN, int MI, int S, int BK = 64>
 hipError_t launch_dlds(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
                        int k, int epi, void* out, hipStream_t st, int group_m) {
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x,
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_BF16, BK>), grid, block, 0, st, x,
                                w, bias, res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0,
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_GELU_BF16, BK>), grid, block, 0,
                                st, x, w, bias, res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st,
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_RES_F32, BK>), grid, block, 0, st,
                                x, w, bias, res, out, m, n, k, group_m);
             break;
         case kEpiResF32Ffn2:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResF32Ffn2>), grid, block, 0, st, x, w,
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResF32Ffn2, BK>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         default:
@@ -463,17 +465,19 @@ __device__ __forceinline__ void interleave_step() {
     }
 }
 
-template <int BM, int BN, int MI, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_sched_kernel(
+template <int BM, int BN, int WM, int WN, int MI, int EPI>
+__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4))) void gemm_sched_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, const float* __restrict__ bias,
     const float* __restrict__ res, void* __restrict__ out, int M, int N, int K, int group_m) {
     typedef Mfma<MI> MF;
     typedef typename MF::acc_t acc_t;
-    constexpr int TM = BM / 2, TN = BN / 2;
+    constexpr int NW = WM * WN;
+    constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / MI, FN = TN / MI;
     constexpr int KS = kBK / MF::kDepth;   // k-steps per slab (2 for 16x16x32, 4 for 32x32x16)
     constexpr int GROUPS = kWave / MI;     // lane groups along k
-    constexpr int LA = BM / 8 / 4, LB = BN / 8 / 4;  // direct loads per wave per stage
+    constexpr int LA = BM / 8 / NW, LB = BN / 8 / NW;  // direct loads per wave per stage
+    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "rows must split over the waves");
     constexpr int STAGE = (BM + BN) * kBK;
     constexpr int NMF = FM * FN, NRD = FM + FN, NGL = LA + LB;
     static_assert(KS % 2 == 0, "fragment buffers alternate per k-step");
@@ -486,7 +490,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int m0 = tm * BM, n0 = tn * BN;
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int wm = wid >> 1, wn = wid & 1;
+    const int wm = wid / WN, wn = wid % WN;
 
     const uint16_t* ga[LA];
     const uint16_t* gb[LB];
@@ -593,7 +597,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     constexpr int PITCH = ROWB + 16;            // padded LDS row pitch
     constexpr int LPR = ROWB / 16;              // lanes per row on read-back
     constexpr int RPI = kWave / LPR;            // rows per read-back instruction
-    static_assert(4 * 32 * PITCH <= 2 * STAGE * 2, "staging must fit in the stage buffers");
+    static_assert(NW * 32 * PITCH <= 2 * STAGE * 2, "staging must fit in the stage buffers");
     block_sync_lds();  // every wave is done with the stage buffers
     char* stg = reinterpret_cast<char*>(smem) + wid * 32 * PITCH;
 #pragma unroll
@@ -645,25 +649,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
 }
 
-template <int BM, int BN, int MI>
+template <int BM, int BN, int WM, int WN, int MI>
 hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
                         int k, int epi, void* out, hipStream_t st, int group_m) {
-    const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(256);
+    const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w, bias,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w, bias,
                                res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x, w,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         case kEpiResF32Ffn2:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, MI, kEpiResF32Ffn2>), grid, block, 0, st, x, w, bias, res,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResF32Ffn2>), grid, block, 0, st, x, w, bias, res,
                                out, m, n, k, group_m);
             break;
         default:
@@ -709,7 +713,7 @@ hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uin
         case 1: return launch_tile<128, 64, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
         case 14: return launch_dlds<256, 256, 2, 4, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 19: return launch_dlds<128, 128, 2, 2, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
-        case 20: return launch_sched<256, 256, 32>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 21: return launch_sched<256, 256, 2, 4, 32>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         default: return hipErrorInvalidValue;
     }
 }
@@ -717,27 +721,28 @@ hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uin
 int gemm_config_bn(int cfg) {
     switch (cfg) {
         case 1: return 64;
-        case 14: case 20: return 256;
+        case 14: case 21: return 256;
         default: return 128;
     }
 }
 
 // Per-shape choice, from measurements on MI355X over the encoder's GEMM shapes
 // (M = 24K..110K tokens; (N, K) = (3d, d), (d, d), (F, d), (d, F)):
-//   bf16 out, bias only (QKV):      scheduled 256 x 256, 32x32x16 MFMA, staged epilogue
-//   bf16 out, bias + GELU (FFN1):   8-wave 256 x 256 direct-to-LDS
-//   fp32 out, bias + residual:      4-wave 128 x 128 direct-to-LDS (more tiles in flight,
-//                                   better for the HBM-heavy fp32 epilogue)
+//   bf16 out, bias (QKV):            8-wave scheduled 256 x 256, staged epilogue
+//   bf16 out, bias + GELU (FFN1):    8-wave 256 x 256 direct-to-LDS
+//   fp32 out, bias + residual:       4-wave 128 x 128 direct-to-LDS; the 8-wave 256 x 256
+//                                    one when K is long and M large (FFN2 at >= 48K tokens)
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
                        int k, int epi, void* out, hipStream_t st, bool ffn2) {
     if (ffn2 && epi == ELIS_EPI_BIAS_RES_F32) epi = kEpiResF32Ffn2;
     if (m < 1 || n % 64 != 0 || k % kBK != 0 || n < 64 || k < kBK) return hipErrorInvalidValue;
     constexpr int kGroupM = 8;
-    if (n % 256 == 0 && epi == ELIS_EPI_BIAS_BF16) return launch_gemm_config(20, kGroupM, x, w, bias, res, m, n, k, epi, out, st);
-    if (n % 256 == 0 && epi == ELIS_EPI_BIAS_GELU_BF16)
-        return launch_gemm_config(14, kGroupM, x, w, bias, res, m, n, k, epi, out, st);
-    if (n % 128 == 0) return launch_gemm_config(19, kGroupM, x, w, bias, res, m, n, k, epi, out, st);
-    return launch_gemm_config(1, 1, x, w, bias, res, m, n, k, epi, out, st);
+    const bool n256 = n % 256 == 0, n128 = n % 128 == 0;
+    int cfg = n128 ? 19 : 1;
+    if (epi == ELIS_EPI_BIAS_BF16 && n256) cfg = 21;
+    else if (epi == ELIS_EPI_BIAS_GELU_BF16 && n256) cfg = 14;
+    else if ((epi == ELIS_EPI_BIAS_RES_F32 || epi == kEpiResF32Ffn2) && n256 && k >= 2048 && m >= 49152) cfg = 14;
+    return launch_gemm_config(cfg, cfg == 1 ? 1 : kGroupM, x, w, bias, res, m, n, k, epi, out, st);
 }
 
 }  // namespace elis

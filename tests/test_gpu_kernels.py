@@ -218,3 +218,34 @@ def test_attention_flags_bad_cu_without_faulting():
                         stream()))
     st, bits = E.elis_read_status(ws, stream())
     assert st == E.ELIS_EDEVICE and bits & E.ELIS_DEV_BAD_CU
+
+
+@pytest.mark.parametrize("epi", [E.ELIS_EPI_BIAS_RES_F32, E.ELIS_EPI_BIAS_GELU_BF16, E.ELIS_EPI_BIAS_BF16])
+def test_linear_large_m_sampled(epi):
+    """Token counts of the 100-round workload (~50K-110K rows) take other tile configurations;
+    checked on sampled rows (first, last, ragged tail and random ones)."""
+    m, n, k = 50001, 768 if epi == E.ELIS_EPI_BIAS_RES_F32 else 1024, 3072 if epi == E.ELIS_EPI_BIAS_RES_F32 else 768
+    note(f"linear large m={m} n={n} k={k} epi={epi}")
+    rng = np.random.default_rng(epi + 7)
+    xb = f32_to_bf16_bits(rng.standard_normal((m, k), dtype=np.float32))
+    wb = f32_to_bf16_bits((rng.standard_normal((n, k), dtype=np.float32) * 0.05))
+    bias = (rng.standard_normal(n) * 0.1).astype(np.float32)
+    res = rng.standard_normal((m, n), dtype=np.float32)
+    d_x, d_w, d_bias, d_res = dev(xb), dev(wb), dev(bias), dev(res)
+    f32 = epi == E.ELIS_EPI_BIAS_RES_F32
+    out = torch.empty((m, n), dtype=torch.float32 if f32 else torch.int16, device="cuda")
+    ok(E.elis_linear(d_x.data_ptr(), d_w.data_ptr(), d_bias.data_ptr(), d_res.data_ptr() if f32 else None, m, n, k,
+                     epi, out.data_ptr(), stream()))
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 1, m - 1, m - 2, m - 17], rng.integers(0, m, 300)]))
+    x64, w64 = bf16_to_f64(xb[rows]), bf16_to_f64(wb)
+    pre = x64 @ w64.T + bias
+    acc_tol = 1e-5 * (np.abs(x64) @ np.abs(w64).T) + 1e-6
+    if f32:
+        got = out[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+        ref = pre + res[rows]
+        assert np.all(np.abs(got - ref) <= acc_tol + 1e-6 * np.abs(ref))
+    else:
+        got = bf16_to_f64(host_u16(out[torch.from_numpy(rows).cuda()]))
+        ref = oracle.gelu(pre) if epi == E.ELIS_EPI_BIAS_GELU_BF16 else pre
+        assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1.2 * acc_tol)
