@@ -58,18 +58,148 @@ def _source_sha(paths):
     return h.hexdigest()
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_hbm_traffic.md")
+
+# Kernel behind each class at the BERT-base, 64-sequence workload (the GEMM routing picks
+# the tile configuration per shape), and the sources whose text fixes that kernel: a PMC
+# figure is reported only while those sources are unchanged.
+_GEMM_SRC = ["paper_2505_09142_amd/csrc/gemm.hip", "paper_2505_09142_amd/csrc/common.h",
+             "paper_2505_09142_amd/csrc/kernels.h"]
+CLASS_KERNELS = {
+    "gemm_qkv": ("gemm_sched_kernel<256, 256, 2, 4, 32, 0>", _GEMM_SRC),
+    "attention": ("attention_kernel<64>", ["paper_2505_09142_amd/csrc/attention.hip",
+                                           "paper_2505_09142_amd/csrc/common.h"]),
+    "gemm_o": ("gemm_dlds_kernel<128, 128, 2, 2, 32, 2, 2, 64>", _GEMM_SRC),
+    "layernorm": ("layernorm_kernel<3>", ["paper_2505_09142_amd/csrc/norm.hip", "paper_2505_09142_amd/csrc/common.h"]),
+    "gemm_ffn1": ("gemm_dlds_kernel<256, 256, 2, 4, 32, 2, 1, 64>", _GEMM_SRC),
+    "gemm_ffn2": ("gemm_dlds_kernel<128, 128, 2, 2, 32, 2, 3, 64>", _GEMM_SRC),
+}
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
 def _traffic(kernel_class: str):
     """HBM bytes per launch from the committed rocprofv3 PMC summary, if the kernel source is unchanged."""
-    path = os.path.join(ROOT, "profiles", f"{kernel_class}_bert_base_b64_traffic.md")
-    if not os.path.exists(path):
+    if not os.path.exists(TRAFFIC_PROFILE):
         return None
-    m = re.search(r"^traffic:\s*(\{.*\})\s*$", open(path).read(), re.M)
+    m = re.search(r"^traffic\[" + re.escape(kernel_class) + r"\]:\s*(\{.*\})\s*$", open(TRAFFIC_PROFILE).read(), re.M)
     if not m:
         return None
     rec = json.loads(m.group(1))
     if rec.get("source_sha256") != _source_sha(rec.get("sources", [])):
         return None
     return rec.get("per_launch_bytes")
+
+
+def _pmc_per_kernel(csv_path, counter):
+    """Counter values (KiB) per dispatch, grouped by demangled kernel name."""
+    import csv
+    import collections
+    out = collections.defaultdict(list)
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"].replace("elis::(anonymous namespace)::", "").replace("void ", "")
+            out[re.sub(r"\(.*", "", name).strip()].append(float(r["Counter_Value"]))
+    return out
+
+
+def summarize_pmc(fetch_csv, write_csv, copy_mib, workload, commands):
+    """Write the HBM-traffic summary from one FETCH_SIZE and one WRITE_SIZE rocprofv3 pass.
+
+    Each counter is scaled by bytes/KiB-reading of the plain device copy of copy_mib MiB
+    that both passes ran first (the largest copy dispatches of each pass)."""
+    from workloads import WORKLOADS, make_batch
+    w = WORKLOADS[workload]
+    b = make_batch(w)
+    fetch = _pmc_per_kernel(fetch_csv, "FETCH_SIZE")
+    write = _pmc_per_kernel(write_csv, "WRITE_SIZE")
+    nbytes = copy_mib * 2 ** 20
+    cf = sorted(fetch[COPY_KERNEL])[-3:]
+    cw = sorted(write[COPY_KERNEL])[-3:]
+    f_scale = nbytes / (sum(cf) / len(cf) * 1024)
+    w_scale = nbytes / (sum(cw) / len(cw) * 1024)
+    T, d, F = b.total, w.shape.d_model, w.shape.d_ff
+    qkv_b = T * 3 * d * 2
+    mandatory = {  # bytes a launch must move at least once: operands in, results out
+        "gemm_qkv": T * d * 2 + 3 * d * d * 2 + 3 * d * 4 + qkv_b,
+        "attention": qkv_b + T * d * 2,
+        "gemm_o": T * d * 2 + d * d * 2 + d * 4 + T * d * 4 * 2,
+        "layernorm": T * d * (4 + 4 + 2),
+        "gemm_ffn1": T * d * 2 + F * d * 2 + F * 4 + T * F * 2,
+        "gemm_ffn2": T * F * 2 + F * d * 2 + d * 4 + T * d * 4 * 2,
+    }
+    lines = [f"# HBM traffic per launch: {workload} (T = {T:,}), rocprofv3 PMC byte counters", "",
+             "Two passes over the same bench command, one counter each (GPU box, repo root as working tree):", ""]
+    lines += [f"    {c}" for c in commands]
+    lines += ["", f"Scale: before its steps each pass runs a plain device-to-device copy of {copy_mib} MiB "
+              f"three times (`{COPY_KERNEL}`). Counter readings of those copies: FETCH_SIZE "
+              f"{', '.join(f'{v:.0f}' for v in cf)} KiB, WRITE_SIZE {', '.join(f'{v:.0f}' for v in cw)} KiB, "
+              f"for {nbytes / 1024:.0f} KiB moved each way, so bytes = FETCH_SIZE x 1024 x {f_scale:.4f} "
+              f"and WRITE_SIZE x 1024 x {w_scale:.4f}.", "",
+              "| class | kernel | launches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled MB | mandatory MB | ratio |",
+              "|---|---|---:|---:|---:|---:|---:|---:|"]
+    recs = {}
+    for cls, (kname, srcs) in CLASS_KERNELS.items():
+        fv, wv = fetch.get(kname, []), write.get(kname, [])
+        if not fv or not wv:
+            lines.append(f"| {cls} | `{kname}` | 0 | - | - | - | - | - |")
+            continue
+        fk, wk = sum(fv) / len(fv), sum(wv) / len(wv)
+        tb = fk * 1024 * f_scale + wk * 1024 * w_scale
+        lines.append(f"| {cls} | `{kname}` | {len(fv)} | {fk:,.0f} | {wk:,.0f} | {tb / 1e6:,.1f} | "
+                     f"{mandatory[cls] / 1e6:,.1f} | {tb / mandatory[cls]:.2f} |")
+        recs[cls] = {"per_launch_bytes": tb, "fetch_kib": fk, "write_kib": wk, "fetch_scale": f_scale,
+                     "write_scale": w_scale, "mandatory_bytes": mandatory[cls], "kernel": kname,
+                     "sources": srcs, "source_sha256": _source_sha(srcs)}
+    lines += ["", "`ratio` = scaled traffic / mandatory bytes; above 1 means operands were fetched from "
+              "memory more than once (tiles re-read after leaving L2).", "",
+              "Machine-readable records (bench.py reads these; a record whose sources have changed since is ignored):", ""]
+    lines += [f"traffic[{c}]: {json.dumps(r)}" for c, r in recs.items()]
+    with open(TRAFFIC_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {TRAFFIC_PROFILE}")
+
+
+TRACE_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_kernel_trace.md")
+_ROLES = {"seqmap_kernel": "sequence table", "embed_ln_kernel<3>": "embedding + LN",
+          "select_rank_kernel": "ISRTF select", "head_hidden_kernel": "head 768->256 + ReLU",
+          "head_out_kernel": "head 256->1, affine", COPY_KERNEL: "(torch copies)"}
+
+
+def summarize_trace(stats_csv, command, bench_json):
+    """Write the kernel-trace summary from a rocprofv3 --stats kernel_stats.csv and the
+    JSON line bench.py printed in the same run."""
+    import csv
+    rec = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    roles = dict(_ROLES)
+    roles.update({k: c for c, (k, _) in CLASS_KERNELS.items()})
+    rows, avg = [], {}
+    with open(stats_csv) as f:
+        for r in csv.DictReader(f):
+            n = re.sub(r"\(.*", "", r["Name"].replace("elis::(anonymous namespace)::", "").replace("void ", "")).strip()
+            avg[n] = float(r["AverageNs"]) / 1e3
+            rows.append(f"| `{n}` | {roles.get(n, '')} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e3:.1f} | "
+                        f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    rl = rec["roofline"]
+    dom = rl["kernel"]
+    prof_us = avg.get(CLASS_KERNELS[dom][0]) if dom in CLASS_KERNELS else None
+    cfg = rec["config"]
+    steps, warm = rec["steps"], rec["warmup"]
+    lines = [f"# Kernel trace: {cfg['workload'].split(':')[0]} (T = {cfg['total_tokens']:,}), predict + select", "",
+             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             f"{warm + 2 * steps} forward passes were traced ({warm} warm-up + {steps} per-class-timed + {steps} "
+             "timed steps). Table from the `kernel_stats.csv` of that run.", "",
+             "| kernel | class | calls | total µs | avg µs | % of GPU time |", "|---|---|---:|---:|---:|---:|"]
+    lines += rows
+    lines += ["", f"bench.py's own line in that run: {rec['ms_per_step']:.3f} ms per step, {rec['value']:.0f} seqs/s. "
+              f"Dominant class `{dom}`: {rl['avg_launch_us']:.1f} µs per launch by bench.py's live HIP events vs "
+              + (f"{prof_us:.1f} µs" if prof_us else "n/a") + " (rocprofv3 average above); "
+              f"{rl['per_launch_flop'] / 1e9:.1f} GFLOP per launch -> {rl['achieved']:.0f} {rl['unit']} = "
+              f"{100 * rl['frac']:.1f}% of the {rl['peak']:.0f} {rl['unit']} dense bf16 peak."]
+    with open(TRACE_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {TRACE_PROFILE}")
 
 
 def cpu_baseline(w, W, b, seconds: float):
@@ -101,7 +231,22 @@ def main():
     ap.add_argument("--workload", default="bert_base_b64")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run a plain device copy of this many MiB three times before the steps "
+                         "(reference dispatches for PMC byte counters)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the HBM-traffic summary from two rocprofv3 --pmc counter_collection.csv files")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("STATS_CSV", "BENCH_JSON", "COMMAND"),
+                    help="write the kernel-trace summary from a rocprofv3 kernel_stats.csv")
+    ap.add_argument("--pmc-command", action="append", default=[],
+                    help="with --summarize-pmc: the command of each pass, recorded in the summary")
     args = ap.parse_args()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace[0], args.summarize_trace[2], args.summarize_trace[1])
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.copy_calibration_mib, args.workload, args.pmc_command)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the hot path is single-GPU by design); got --gpus {args.gpus}",
               file=sys.stderr)
@@ -129,6 +274,14 @@ def main():
     def step():
         pr.predict(ids, cu, msl, out_pred=pred)
         pr.select(pred, arr, w.batch_cap, out_idx, out_cnt)
+
+    if args.copy_calibration_mib:
+        src = torch.ones(args.copy_calibration_mib * 2 ** 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         step()

@@ -375,32 +375,51 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
         }
     }
 
+    // Epilogue. Loads are batched ahead of their use: the bias vectors of this lane's
+    // columns once, and a block row's residual vectors all together, so the latency of
+    // global loads is paid once per block row instead of once per output vector.
+    constexpr int NQ = MF::kRegs / 4;  // 4-column groups per MFMA block per lane
+    constexpr bool F32OUT = (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2);
+    f32x4 bv[FN][NQ];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+            bv[j][q] = *reinterpret_cast<const f32x4*>(bias + n0 + wn * TN + j * MI + 8 * q + 4 * kg);
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int m = m0 + wm * TM + i * MI + rl;
+        const int mc = m < M ? m : M - 1;  // rows past the end load a valid row, store nothing
+        const size_t ro = static_cast<size_t>(mc) * N + n0 + wn * TN + 4 * kg;
+        f32x4 rv[FN][NQ];
+        if constexpr (F32OUT) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) rv[j][q] = *reinterpret_cast<const f32x4*>(res + ro + j * MI + 8 * q);
+        }
         if (m >= M) continue;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
 #pragma unroll
-            for (int q = 0; q < MF::kRegs / 4; ++q) {
-                const int n = n0 + wn * TN + j * MI + 8 * q + 4 * kg;
+            for (int q = 0; q < NQ; ++q) {
                 f32x4 v;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
-                v += *reinterpret_cast<const f32x4*>(bias + n);
-                const size_t o = static_cast<size_t>(m) * N + n;
-                if constexpr (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2) {
-                    v += *reinterpret_cast<const f32x4*>(res + o);
+                v += bv[j][q];
+                const size_t o = ro + j * MI + 8 * q;
+                if constexpr (F32OUT) {
+                    v += rv[j][q];
                     *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
                 } else {
                     if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
 #pragma unroll
                         for (int c = 0; c < 4; ++c) v[c] = gelu_erf(v[c]);
                     }
-                    u32x2 p;
-                    p[0] = pack_bf16x2(v[0], v[1]);
-                    p[1] = pack_bf16x2(v[2], v[3]);
-                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + o) = p;
+                    u32x2 pk;
+                    pk[0] = pack_bf16x2(v[0], v[1]);
+                    pk[1] = pack_bf16x2(v[2], v[3]);
+                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + o) = pk;
                 }
             }
         }
