@@ -226,7 +226,7 @@ def cpu_baseline(w, W, b, seconds: float):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="bert_base_b64")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)

@@ -45,23 +45,25 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblk) {
     return xcd * per + (xcd < rem ? xcd : rem) + local;
 }
 
-// GELU(x) = x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf from Abramowitz & Stegun 7.1.26:
-// for z >= 0, erfc(z) = (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2) + e(z),
-// t = 1 / (1 + p z), |e(z)| <= 1.5e-7. Branch-free: one reciprocal, one exp2, five FMAs.
 // LDS chunk swizzle of the direct-to-LDS kernels: physical 16-byte chunk = logical chunk ^ swz(row).
 // Measured free of bank conflicts on gfx950 for both 16-row and 32-row fragment reads (the
 // plain row & 7 form conflicts 4-way on 32-row reads).
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
+// GELU(x) = x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf from Abramowitz & Stegun 7.1.26:
+// for z >= 0, erfc(z) = (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2) + e(z),
+// t = 1 / (1 + p z), |e(z)| <= 1.5e-7. Since erf is odd, x * Phi(x) = max(x, 0) - |x| * h with
+// h = erfc(|x| / sqrt 2) / 2, so no branch or select on the sign: one reciprocal, one exp2,
+// six FMAs and four multiplies (the 1/2 and 1/sqrt 2 are folded into the constants).
 __device__ __forceinline__ float gelu_erf(float x) {
-    constexpr float p = 0.3275911f;
-    constexpr float a1 = 0.254829592f, a2 = -0.284496736f, a3 = 1.421413741f, a4 = -1.453152027f,
-                    a5 = 1.061405429f;
-    const float z = fabsf(x) * 0.70710678118654752f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(p, z, 1.0f));
+    constexpr float p = 0.3275911f * 0.70710678118654752f;
+    constexpr float a1 = 0.5f * 0.254829592f, a2 = 0.5f * -0.284496736f, a3 = 0.5f * 1.421413741f,
+                    a4 = 0.5f * -1.453152027f, a5 = 0.5f * 1.061405429f;
+    const float ax = fabsf(x);
+    const float t = __builtin_amdgcn_rcpf(fmaf(p, ax, 1.0f));
     const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, a5, a4), a3), a2), a1);
-    const float tail = poly * __builtin_amdgcn_exp2f(-z * z * 1.4426950408889634f);  // erfc(|x|/sqrt 2)
-    return 0.5f * x * (x >= 0.f ? 2.0f - tail : tail);
+    const float h = poly * __builtin_amdgcn_exp2f((x * x) * -0.72134752044448170f);  // exp(-x^2 / 2)
+    return fmaf(-ax, h, fmaxf(x, 0.f));
 }
 
 // One MFMA block of the wave tile: MI x MI outputs (MI = 16: 16x16x32, MI = 32: 32x32x16).
@@ -484,8 +486,8 @@ __device__ __forceinline__ void interleave_step() {
     }
 }
 
-template <int BM, int BN, int WM, int WN, int MI, int EPI>
-__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4))) void gemm_sched_kernel(
+template <int BM, int BN, int WM, int WN, int MI, int EPI, int BK = 64, int OCC = 1, int S = 2>
+__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void gemm_sched_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, const float* __restrict__ bias,
     const float* __restrict__ res, void* __restrict__ out, int M, int N, int K, int group_m) {
     typedef Mfma<MI> MF;
@@ -493,14 +495,18 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(W
     constexpr int NW = WM * WN;
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / MI, FN = TN / MI;
-    constexpr int KS = kBK / MF::kDepth;   // k-steps per slab (2 for 16x16x32, 4 for 32x32x16)
+    constexpr int KS = BK / MF::kDepth;    // k-steps per slab
     constexpr int GROUPS = kWave / MI;     // lane groups along k
-    constexpr int LA = BM / 8 / NW, LB = BN / 8 / NW;  // direct loads per wave per stage
-    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "rows must split over the waves");
-    constexpr int STAGE = (BM + BN) * kBK;
+    constexpr int CPR = BK / 8;            // 16-byte chunks per slab row
+    constexpr int RPI = kWave / CPR;       // slab rows covered by one wave-wide 16-byte load
+    constexpr int SWS = BK == 64 ? 1 : 2;  // swizzle: chunk ^ ((row >> SWS) & (CPR - 1))
+    constexpr int LA = BM / RPI / NW, LB = BN / RPI / NW;  // direct loads per wave per stage
+    static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "rows must split over the waves");
+    constexpr int STAGE = (BM + BN) * BK;
     constexpr int NMF = FM * FN, NRD = FM + FN, NGL = LA + LB;
     static_assert(KS % 2 == 0, "fragment buffers alternate per k-step");
-    __shared__ __attribute__((aligned(1024))) uint16_t smem[2 * STAGE];
+    static_assert(S >= 2 && S * NGL < 64, "pipeline depth");
+    __shared__ __attribute__((aligned(1024))) uint16_t smem[S * STAGE];
 
     const int tiles_n = N / BN;
     const int tiles_m = (M + BM - 1) / BM;
@@ -510,38 +516,39 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(W
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int wm = wid / WN, wn = wid % WN;
+    auto sw = [](int row) { return (row >> SWS) & (CPR - 1); };
 
     const uint16_t* ga[LA];
     const uint16_t* gb[LB];
 #pragma unroll
     for (int i = 0; i < LA; ++i) {
-        const int row = (wid * LA + i) * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ swz(row);
+        const int row = (wid * LA + i) * RPI + lane / CPR;
+        const int c = (lane % CPR) ^ sw(row);
         const int gr = (m0 + row < M) ? m0 + row : M - 1;
         ga[i] = A + static_cast<size_t>(gr) * K + c * 8;
     }
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
-        const int row = (wid * LB + i) * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ swz(row);
+        const int row = (wid * LB + i) * RPI + lane / CPR;
+        const int c = (lane % CPR) ^ sw(row);
         gb[i] = B + static_cast<size_t>(n0 + row) * K + c * 8;
     }
     auto issue = [&](int kt) {
-        uint16_t* st = smem + (kt & 1) * STAGE;
-        const int k0 = kt * kBK;
+        uint16_t* st = smem + (kt % S) * STAGE;
+        const int k0 = kt * BK;
 #pragma unroll
-        for (int i = 0; i < LA; ++i) load_lds_16(ga[i] + k0, st + (wid * LA + i) * 8 * kBK);
+        for (int i = 0; i < LA; ++i) load_lds_16(ga[i] + k0, st + (wid * LA + i) * RPI * BK);
 #pragma unroll
-        for (int i = 0; i < LB; ++i) load_lds_16(gb[i] + k0, st + BM * kBK + (wid * LB + i) * 8 * kBK);
+        for (int i = 0; i < LB; ++i) load_lds_16(gb[i] + k0, st + BM * BK + (wid * LB + i) * RPI * BK);
     };
 
     const int rl = lane % MI, kg = lane / MI;
     int offa[FM], offb[FN];
 #pragma unroll
-    for (int i = 0; i < FM; ++i) offa[i] = (wm * TM + i * MI + rl) * kBK;
+    for (int i = 0; i < FM; ++i) offa[i] = (wm * TM + i * MI + rl) * BK;
 #pragma unroll
-    for (int j = 0; j < FN; ++j) offb[j] = BM * kBK + (wn * TN + j * MI + rl) * kBK;
-    const int rs = swz(rl);  // fragment rows start at multiples of 16, so swz(row) == swz(rl)
+    for (int j = 0; j < FN; ++j) offb[j] = BM * BK + (wn * TN + j * MI + rl) * BK;
+    const int rs = sw(rl);  // fragment rows start at multiples of 16, so sw(row) == sw(rl)
 
     bf16x8 fa[2][FM], fb[2][FN];
     auto load_frags = [&](int buf, int stage, int ks) {
@@ -568,22 +575,23 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(W
             for (int j = 0; j < FN; ++j) acc[i][j] = MF::run(fb[buf][j], fa[buf][i], acc[i][j]);
     };
 
-    const int KT = K / kBK;
-    issue(0);
-    if (KT > 1) {
-        issue(1);
-        wait_vmcnt<NGL>();
-    } else {
-        wait_vmcnt<0>();
-    }
+    const int KT = K / BK;
+    // Prologue: every stage gets a slab (slabs 0 .. S-1); wait for slab 0 only.
+#pragma unroll
+    for (int p = 0; p < S; ++p)
+        if (p < KT) issue(p);
+    if (KT >= S) wait_vmcnt<(S - 1) * NGL>();
+    else wait_vmcnt<0>();
     block_sync_lds();
     load_frags(0, 0, 0);
 
-    // One slab. ISSUE: request slab kt+2; NEXT: slab kt+1 exists (read its first fragments).
-    // Both are compile-time so the steady-state loop is straight-line code.
-    auto slab = [&](int kt, auto issue_c, auto next_c) {
+    // One slab. WAIT: slabs still allowed in flight once slab kt+1 has landed; ISSUE: request
+    // slab kt+S into the stage slab kt frees; NEXT: slab kt+1 exists (read its first
+    // fragments). All compile-time, so the steady-state loop is straight-line code.
+    auto slab = [&](int kt, auto wait_c, auto issue_c, auto next_c) {
+        constexpr int WAIT = decltype(wait_c)::value;
         constexpr bool ISSUE = decltype(issue_c)::value, NEXT = decltype(next_c)::value;
-        const int cur = kt & 1;
+        const int cur = kt % S;
 #pragma unroll
         for (int ks = 0; ks < KS - 1; ++ks) {
             load_frags((ks + 1) & 1, cur, ks + 1);
@@ -591,20 +599,22 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(W
             interleave_step<0, NMF, 0, NRD, 0>();
         }
         // Slab kt+1 has landed and every wave's reads of stage `cur` are complete.
-        wait_vmcnt<0>();
+        wait_vmcnt<WAIT * NGL>();
         wait_lgkm<0>();
         block_sync_lds();
-        if constexpr (ISSUE) issue(kt + 2);
-        if constexpr (NEXT) load_frags(0, cur ^ 1, 0);
+        if constexpr (ISSUE) issue(kt + S);
+        if constexpr (NEXT) load_frags(0, (kt + 1) % S, 0);
         mfma_all((KS - 1) & 1);
         interleave_step<0, NMF, ISSUE ? NGL : 0, NEXT ? NRD : 0, 1>();
     };
     typedef std::integral_constant<bool, true> T_;
     typedef std::integral_constant<bool, false> F_;
+    typedef std::integral_constant<int, S - 2> WS_;
+    typedef std::integral_constant<int, 0> W0_;
     int kt = 0;
-    for (; kt + 2 < KT; ++kt) slab(kt, T_(), T_());
-    if (kt + 1 < KT) slab(kt++, F_(), T_());
-    slab(kt, F_(), F_());
+    for (; kt + S < KT; ++kt) slab(kt, WS_(), T_(), T_());
+    for (; kt + 1 < KT; ++kt) slab(kt, W0_(), F_(), T_());
+    slab(kt, W0_(), F_(), F_());
 
     // Epilogue through LDS: each wave stages one 32-row block row of its output tile (bias,
     // activation / residual applied), then writes it back as whole rows, 16 bytes per lane,
@@ -615,8 +625,8 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(W
     constexpr int ROWB = TN * EB;               // bytes of one wave-tile row
     constexpr int PITCH = ROWB + 16;            // padded LDS row pitch
     constexpr int LPR = ROWB / 16;              // lanes per row on read-back
-    constexpr int RPI = kWave / LPR;            // rows per read-back instruction
-    static_assert(NW * 32 * PITCH <= 2 * STAGE * 2, "staging must fit in the stage buffers");
+    constexpr int RPR = kWave / LPR;            // rows per read-back instruction
+    static_assert(NW * 32 * PITCH <= S * STAGE * 2, "staging must fit in the stage buffers");
     block_sync_lds();  // every wave is done with the stage buffers
     char* stg = reinterpret_cast<char*>(smem) + wid * 32 * PITCH;
 #pragma unroll
@@ -648,8 +658,8 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(W
         __builtin_amdgcn_wave_barrier();
         asm volatile("" ::: "memory");
 #pragma unroll
-        for (int rr = 0; rr < 32 / RPI; ++rr) {
-            const int row = rr * RPI + lane / LPR, ch = lane % LPR;
+        for (int rr = 0; rr < 32 / RPR; ++rr) {
+            const int row = rr * RPR + lane / LPR, ch = lane % LPR;
             const int m = m0 + wm * TM + i * MI + row;
             const u32x4 d = *reinterpret_cast<const u32x4*>(stg + row * PITCH + ch * 16);
             if (m < M) {
@@ -668,25 +678,25 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(W
     }
 }
 
-template <int BM, int BN, int WM, int WN, int MI>
+template <int BM, int BN, int WM, int WN, int MI, int BK = 64, int OCC = 1, int S = 2>
 hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
                         int k, int epi, void* out, hipStream_t st, int group_m) {
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w, bias,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16, BK, OCC, S>), grid, block, 0, st, x, w, bias,
                                res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x, w,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16, BK, OCC, S>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, BK, OCC, S>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         case kEpiResF32Ffn2:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResF32Ffn2>), grid, block, 0, st, x, w, bias, res,
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResF32Ffn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
                                out, m, n, k, group_m);
             break;
         default:
