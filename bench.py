@@ -40,10 +40,11 @@ def _algorithmic(w, b):
         "gemm_o": ("flop", 2.0 * T * d * d, L),
         "gemm_ffn1": ("flop", 2.0 * T * d * F, L),
         "gemm_ffn2": ("flop", 2.0 * T * F * d, L),
-        # fp32 row in; fp32 + bf16 rows out (the last LayerNorm writes fp32 only: counted as the common case)
-        "layernorm": ("byte", T * d * (4.0 + 4.0 + 2.0), 2 * L),
-        # ids + gathered bf16 word and position rows in; fp32 + bf16 rows out
-        "embed_ln": ("byte", T * (4.0 + d * (2.0 + 2.0 + 4.0 + 2.0)), 1),
+        # fp32 row in; bf16 row + (mean, rstd) out (the last LayerNorm writes an fp32 row instead:
+        # counted as the common case)
+        "layernorm": ("byte", T * (d * (4.0 + 2.0) + 8.0), 2 * L),
+        # ids + gathered bf16 word and position rows in; fp32 pre-norm + bf16 rows + stats out
+        "embed_ln": ("byte", T * (4.0 + d * (2.0 + 2.0 + 4.0 + 2.0) + 8.0), 1),
         "pool_head": ("byte", n * d * 4.0 + (s.head_hidden or 1) * d * 4.0, 1),
         "seqmap": ("byte", (n + 1) * 4.0 * 4, 1),
         "select": ("byte", n * 12.0 + w.batch_cap * 4.0, 1),
@@ -66,13 +67,13 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_hbm_traffic.md")
 _GEMM_SRC = ["paper_2505_09142_amd/csrc/gemm.hip", "paper_2505_09142_amd/csrc/common.h",
              "paper_2505_09142_amd/csrc/kernels.h"]
 CLASS_KERNELS = {
-    "gemm_qkv": ("gemm_sched_kernel<256, 256, 2, 4, 32, 0>", _GEMM_SRC),
+    "gemm_qkv": ("gemm_sched_kernel<256, 256, 2, 4, 32, 0, 64, 1, 2>", _GEMM_SRC),
     "attention": ("attention_kernel<64>", ["paper_2505_09142_amd/csrc/attention.hip",
                                            "paper_2505_09142_amd/csrc/common.h"]),
-    "gemm_o": ("gemm_dlds_kernel<128, 128, 2, 2, 32, 2, 2, 64>", _GEMM_SRC),
+    "gemm_o": ("gemm_sched_kernel<128, 128, 2, 2, 32, 4, 64, 2, 2>", _GEMM_SRC),
     "layernorm": ("layernorm_kernel<3>", ["paper_2505_09142_amd/csrc/norm.hip", "paper_2505_09142_amd/csrc/common.h"]),
     "gemm_ffn1": ("gemm_dlds_kernel<256, 256, 2, 4, 32, 2, 1, 64>", _GEMM_SRC),
-    "gemm_ffn2": ("gemm_dlds_kernel<128, 128, 2, 2, 32, 2, 3, 64>", _GEMM_SRC),
+    "gemm_ffn2": ("gemm_sched_kernel<128, 128, 2, 2, 32, 5, 64, 2, 2>", _GEMM_SRC),
 }
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
@@ -124,10 +125,10 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, workload, commands):
     mandatory = {  # bytes a launch must move at least once: operands in, results out
         "gemm_qkv": T * d * 2 + 3 * d * d * 2 + 3 * d * 4 + qkv_b,
         "attention": qkv_b + T * d * 2,
-        "gemm_o": T * d * 2 + d * d * 2 + d * 4 + T * d * 4 * 2,
-        "layernorm": T * d * (4 + 4 + 2),
+        "gemm_o": T * d * 2 + d * d * 2 + d * 4 * 3 + T * 8 + T * d * 4 * 2,
+        "layernorm": T * (d * (4 + 2) + 8),
         "gemm_ffn1": T * d * 2 + F * d * 2 + F * 4 + T * F * 2,
-        "gemm_ffn2": T * F * 2 + F * d * 2 + d * 4 + T * d * 4 * 2,
+        "gemm_ffn2": T * F * 2 + F * d * 2 + d * 4 * 3 + T * 8 + T * d * 4 * 2,
     }
     lines = [f"# HBM traffic per launch: {workload} (T = {T:,}), rocprofv3 PMC byte counters", "",
              "Two passes over the same bench command, one counter each (GPU box, repo root as working tree):", ""]

@@ -91,7 +91,8 @@ bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) =
 
 // ------------------------------------------------------------------ workspace layout
 struct PredictLayout {
-    size_t status, start, len, tile_off, x32, xb, qkv, attn, h32, ffn, pool_partial, pool_z, head_hid, total;
+    size_t status, start, len, tile_off, x32, xb, qkv, attn, ha, hb, sa, sb, ffn, pool_partial, pool_z, head_hid,
+        total;
     int nchunk;
 };
 
@@ -113,7 +114,10 @@ PredictLayout predict_layout(const elis_config& c, int T, int n, int max_seqlen)
         p.xb = take(2 * t * d);
         p.qkv = take(2 * t * 3 * d);
         p.attn = take(2 * t * d);
-        p.h32 = take(4 * t * d);
+        p.ha = take(4 * t * d);
+        p.hb = take(4 * t * d);
+        p.sa = take(sizeof(float2) * t);
+        p.sb = take(sizeof(float2) * t);
         p.ffn = take(2 * t * F);
     }
     p.nchunk = (max_seqlen + kPoolChunk - 1) / kPoolChunk;
@@ -185,47 +189,60 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
     uint16_t* xb = L ? at<uint16_t>(workspace, p.xb) : nullptr;
     uint16_t* qkv = L ? at<uint16_t>(workspace, p.qkv) : nullptr;
     uint16_t* attn = L ? at<uint16_t>(workspace, p.attn) : nullptr;
-    float* h32 = L ? at<float>(workspace, p.h32) : nullptr;
+    // Pre-norm rows of the two sub-blocks (fp32) and their (mean, rstd): hb/sb hold the
+    // embedding sum and then each layer's FFN output, ha/sa the attention sub-block's.
+    float* ha = L ? at<float>(workspace, p.ha) : nullptr;
+    float* hb = L ? at<float>(workspace, p.hb) : nullptr;
+    float2* sa = L ? at<float2>(workspace, p.sa) : nullptr;
+    float2* sb = L ? at<float2>(workspace, p.sb) : nullptr;
     uint16_t* ffn = L ? at<uint16_t>(workspace, p.ffn) : nullptr;
 
     hipError_t e;
     e = timed(ELIS_K_SEQMAP, st, [&] { return launch_seqmap(cu_seqlens, n, T, max_seqlen, tab, status, st); });
     if (e != hipSuccess) return status_of(e);
     e = timed(ELIS_K_EMBED_LN, st, [&] {
+        const LnOut o = L ? LnOut{nullptr, xb, hb, sb} : LnOut{final32, nullptr, nullptr, nullptr};
         return launch_embed_ln(token_ids, cu_seqlens, n, T, w->word, w->pos, w->type0, w->emb_ln_g, w->emb_ln_b, d,
-                               c.vocab, c.max_pos, c.ln_eps, L ? x32 : final32, xb, status, st);
+                               c.vocab, c.max_pos, c.ln_eps, o, status, st);
     });
     if (e != hipSuccess) return status_of(e);
+    // LayerNorm parameters of the row held in hb/sb (the input of the next layer).
+    const float* prev_g = w->emb_ln_g;
+    const float* prev_b = w->emb_ln_b;
     for (int l = 0; l < L; ++l) {
         const elis_layer_weights& y = w->layers[l];
         const bool last = (l == L - 1);
         e = timed(ELIS_K_GEMM_QKV, st, [&] {
-            return launch_gemm(xb, y.w_qkv, y.b_qkv, nullptr, T, 3 * d, d, ELIS_EPI_BIAS_BF16, qkv, st);
+            return launch_gemm(xb, y.w_qkv, y.b_qkv, Residual{}, T, 3 * d, d, ELIS_EPI_BIAS_BF16, qkv, st);
         });
         if (e != hipSuccess) return status_of(e);
         e = timed(ELIS_K_ATTENTION, st,
                   [&] { return launch_attention(qkv, tab, n, T, c.n_heads, d / c.n_heads, attn, st); });
         if (e != hipSuccess) return status_of(e);
         e = timed(ELIS_K_GEMM_O, st, [&] {
-            return launch_gemm(attn, y.w_o, y.b_o, x32, T, d, d, ELIS_EPI_BIAS_RES_F32, h32, st);
-        });
-        if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_LAYERNORM, st,
-                  [&] { return launch_layernorm(h32, y.ln1_g, y.ln1_b, T, d, c.ln_eps, x32, xb, st); });
-        if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_GEMM_FFN1, st, [&] {
-            return launch_gemm(xb, y.w_1, y.b_1, nullptr, T, F, d, ELIS_EPI_BIAS_GELU_BF16, ffn, st);
-        });
-        if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_GEMM_FFN2, st, [&] {
-            return launch_gemm(ffn, y.w_2, y.b_2, x32, T, d, F, ELIS_EPI_BIAS_RES_F32, h32, st, true);
+            return launch_gemm(attn, y.w_o, y.b_o, Residual{hb, sb, prev_g, prev_b}, T, d, d, kEpiResLn, ha, st);
         });
         if (e != hipSuccess) return status_of(e);
         e = timed(ELIS_K_LAYERNORM, st, [&] {
-            return launch_layernorm(h32, y.ln2_g, y.ln2_b, T, d, c.ln_eps, last ? final32 : x32,
-                                    last ? nullptr : xb, st);
+            return launch_layernorm(ha, y.ln1_g, y.ln1_b, T, d, c.ln_eps, LnOut{nullptr, xb, nullptr, sa}, st);
         });
         if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_GEMM_FFN1, st, [&] {
+            return launch_gemm(xb, y.w_1, y.b_1, Residual{}, T, F, d, ELIS_EPI_BIAS_GELU_BF16, ffn, st);
+        });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_GEMM_FFN2, st, [&] {
+            return launch_gemm(ffn, y.w_2, y.b_2, Residual{ha, sa, y.ln1_g, y.ln1_b}, T, d, F, kEpiResLnFfn2, hb,
+                               st);
+        });
+        if (e != hipSuccess) return status_of(e);
+        e = timed(ELIS_K_LAYERNORM, st, [&] {
+            const LnOut o = last ? LnOut{final32, nullptr, nullptr, nullptr} : LnOut{nullptr, xb, nullptr, sb};
+            return launch_layernorm(hb, y.ln2_g, y.ln2_b, T, d, c.ln_eps, o, st);
+        });
+        if (e != hipSuccess) return status_of(e);
+        prev_g = y.ln2_g;
+        prev_b = y.ln2_b;
     }
     e = timed(ELIS_K_POOL_HEAD, st, [&] {
         const PoolScratch scr{c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_partial) : nullptr,
@@ -281,7 +298,8 @@ int elis_linear(const uint16_t* x, const uint16_t* w, const float* bias, const f
     const int cls = epilogue == ELIS_EPI_BIAS_GELU_BF16 ? ELIS_K_GEMM_FFN1
                     : epilogue == ELIS_EPI_BIAS_RES_F32 ? ELIS_K_GEMM_FFN2
                                                         : ELIS_K_GEMM_QKV;
-    return status_of(timed(cls, st, [&] { return launch_gemm(x, w, bias, residual, m, n, k, epilogue, out, st); }));
+    const Residual res{epilogue == ELIS_EPI_BIAS_RES_F32 ? residual : nullptr, nullptr, nullptr, nullptr};
+    return status_of(timed(cls, st, [&] { return launch_gemm(x, w, bias, res, m, n, k, epilogue, out, st); }));
 }
 
 size_t elis_attention_workspace_bytes(int32_t n_seqs, int32_t total_tokens) {
@@ -323,7 +341,8 @@ int elis_layernorm(const float* x, const float* g, const float* b, int32_t rows,
     if (d % 64 || d > 2048) return ELIS_EUNSUPPORTED;
     hipStream_t st = static_cast<hipStream_t>(stream);
     return status_of(
-        timed(ELIS_K_LAYERNORM, st, [&] { return launch_layernorm(x, g, b, rows, d, eps, out_f32, out_bf16, st); }));
+        timed(ELIS_K_LAYERNORM, st,
+              [&] { return launch_layernorm(x, g, b, rows, d, eps, LnOut{out_f32, out_bf16, nullptr, nullptr}, st); }));
 }
 
 int elis_timing_enable(uint32_t class_mask) {

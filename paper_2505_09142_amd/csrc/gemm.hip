@@ -2,18 +2,23 @@
 //   out[m, n] = epilogue( sum_k x[m, k] * w[n, k] + bias[n] )
 // x is the activation, bf16 [M, K] row-major; w is the weight, bf16 [N, K]
 // row-major ([out, in]); both operands are K-contiguous. fp32 accumulation.
+// Epilogues: bf16 out; bf16 out after GELU; fp32 out plus a residual, which is
+// either an fp32 matrix or a LayerNorm output rebuilt from its pre-norm rows and
+// row statistics (Residual in kernels.h).
 //
-// Tiling. A work-group computes a BM x BN tile with WM x WN waves; each wave
-// owns a (BM/WM) x (BN/WN) sub-tile made of 16 x 16 MFMA blocks
-// (v_mfma_f32_16x16x32_bf16: 16 x 16 output, 32-deep k per instruction).
-// K advances in steps of 64 through two LDS stages: while the waves multiply
-// out of one stage, the next k-slab is already in flight from HBM into
-// registers and is written to the other stage afterwards (one barrier per
-// k-step).
+// Three kernel families, chosen per shape by launch_gemm:
+//   gemm_kernel        register-staged k-slabs, 16 x 16 x 32 MFMA blocks; covers
+//                      N that is a multiple of 64 only;
+//   gemm_dlds_kernel   k-slabs go HBM -> LDS with global_load_lds_dwordx4 (no
+//                      register staging), S stages, 32 x 32 x 16 MFMA blocks;
+//   gemm_sched_kernel  the same loads plus a hand-scheduled k-loop: operand
+//                      fragments double-buffered in registers, MFMAs of the last
+//                      k-step of a slab issued after the slab barrier, and an
+//                      epilogue staged through LDS for full-line stores.
 //
-// LDS layout. A k-slab row is 64 bf16 = 128 bytes = eight 16-byte chunks; the
-// chunk index is XOR-swizzled with the row (chunk ^ (row & 7)) so the 16 rows
-// that one MFMA operand read touches fall on different banks.
+// LDS layout. A k-slab row of 64 bf16 is eight 16-byte chunks; the chunk index
+// is XOR-swizzled with the row so the rows one MFMA operand read touches fall on
+// different banks (see swz).
 //
 // Operand order. The MFMA is issued as (weight fragment, activation
 // fragment), which computes the transposed tile: lane l then holds 4
@@ -23,8 +28,8 @@
 //
 // Work-group order. The hardware hands consecutive work-group ids round-robin
 // to the 8 XCDs (each with its own L2). Ids are remapped so every XCD gets one
-// contiguous range of tiles, ordered N-fastest: the tiles an XCD runs together
-// share their activation rows, which are then fetched from HBM once per XCD.
+// contiguous range of tiles, grouped GROUP_M tile rows at a time: the tiles an
+// XCD runs together share activation rows and weight columns in its L2.
 #include <type_traits>
 
 #include "kernels.h"
@@ -34,9 +39,25 @@ namespace elis {
 namespace {
 
 constexpr int kBK = 64;
-// Same arithmetic as ELIS_EPI_BIAS_RES_F32; a separate instantiation so that the
-// second feed-forward product shows up under its own kernel name in profiles.
-constexpr int kEpiResF32Ffn2 = 3;
+
+template <int EPI>
+constexpr bool kF32Out = EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResLn || EPI == kEpiResLnFfn2;
+template <int EPI>
+constexpr bool kResLn = EPI == kEpiResLn || EPI == kEpiResLnFfn2;
+constexpr bool kResLnCode(int epi) { return epi == kEpiResLn || epi == kEpiResLnFfn2; }
+
+// Residual of 4 consecutive columns n..n+3 of row m, given the 4 values h of res.x there.
+template <int EPI>
+__device__ __forceinline__ f32x4 residual4(const Residual& res, f32x4 h, int m, int n) {
+    if constexpr (kResLn<EPI>) {
+        const float2 st = res.stats[m];
+        const f32x4 g = *reinterpret_cast<const f32x4*>(res.g + n);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(res.b + n);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) h[c] = fmaf((h[c] - st.x) * st.y, g[c], b[c]);
+    }
+    return h;
+}
 
 __device__ __forceinline__ int xcd_remap(int bid, int nblk) {
     constexpr int kXcd = 8;
@@ -94,7 +115,7 @@ template <int BM, int BN, int WM, int WN, int MI, int EPI>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __restrict__ A,
                                                              const uint16_t* __restrict__ B,
                                                              const float* __restrict__ bias,
-                                                             const float* __restrict__ res, void* __restrict__ out,
+                                                             Residual res, void* __restrict__ out,
                                                              int M, int N, int K) {
     typedef Mfma<MI> MF;
     typedef typename MF::acc_t acc_t;
@@ -206,8 +227,8 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __r
                 for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
                 v += *reinterpret_cast<const f32x4*>(bias + n);
                 const size_t o = static_cast<size_t>(m) * N + n;
-                if constexpr (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2) {
-                    v += *reinterpret_cast<const f32x4*>(res + o);
+                if constexpr (kF32Out<EPI>) {
+                    v += residual4<EPI>(res, *reinterpret_cast<const f32x4*>(res.x + o), m, n);
                     *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
                 } else {
                     if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
@@ -267,7 +288,7 @@ template <int BM, int BN, int WM, int WN, int MI, int S, int EPI, int BK = 64>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t* __restrict__ A,
                                                                   const uint16_t* __restrict__ B,
                                                                   const float* __restrict__ bias,
-                                                                  const float* __restrict__ res,
+                                                                  Residual res,
                                                                   void* __restrict__ out, int M, int N, int K,
                                                                   int group_m) {
     typedef Mfma<MI> MF;
@@ -377,43 +398,80 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
         }
     }
 
-    // Epilogue. Loads are batched ahead of their use: the bias vectors of this lane's
-    // columns once, and a block row's residual vectors all together, so the latency of
-    // global loads is paid once per block row instead of once per output vector.
+    // Epilogue. Loads are batched ahead of their use, so their latency is paid once per
+    // batch instead of once per output vector. Lane (rl, kg) holds, for row m = rl of block
+    // row i, groups of 4 consecutive columns at 8 * q + 4 * kg of block column j.
     constexpr int NQ = MF::kRegs / 4;  // 4-column groups per MFMA block per lane
-    constexpr bool F32OUT = (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2);
-    f32x4 bv[FN][NQ];
+    if constexpr (kF32Out<EPI>) {
+        // fp32 out: one block column at a time. Its bias (and LayerNorm g, b) vectors are
+        // requested together, then per block row the residual vectors of that row.
+        float2 stv[FM];
+        if constexpr (kResLn<EPI>) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int q = 0; q < NQ; ++q)
-            bv[j][q] = *reinterpret_cast<const f32x4*>(bias + n0 + wn * TN + j * MI + 8 * q + 4 * kg);
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = m0 + wm * TM + i * MI + rl;
-        const int mc = m < M ? m : M - 1;  // rows past the end load a valid row, store nothing
-        const size_t ro = static_cast<size_t>(mc) * N + n0 + wn * TN + 4 * kg;
-        f32x4 rv[FN][NQ];
-        if constexpr (F32OUT) {
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-#pragma unroll
-                for (int q = 0; q < NQ; ++q) rv[j][q] = *reinterpret_cast<const f32x4*>(res + ro + j * MI + 8 * q);
+            for (int i = 0; i < FM; ++i) {
+                const int m = m0 + wm * TM + i * MI + rl;
+                stv[i] = res.stats[m < M ? m : M - 1];
+            }
         }
-        if (m >= M) continue;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
+            const int nj = n0 + wn * TN + j * MI + 4 * kg;
+            f32x4 bj[NQ], gj[NQ], ej[NQ];
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
-                f32x4 v;
+                bj[q] = *reinterpret_cast<const f32x4*>(bias + nj + 8 * q);
+                if constexpr (kResLn<EPI>) {
+                    gj[q] = *reinterpret_cast<const f32x4*>(res.g + nj + 8 * q);
+                    ej[q] = *reinterpret_cast<const f32x4*>(res.b + nj + 8 * q);
+                }
+            }
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
-                v += bv[j][q];
-                const size_t o = ro + j * MI + 8 * q;
-                if constexpr (F32OUT) {
-                    v += rv[j][q];
-                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
-                } else {
+            for (int i = 0; i < FM; ++i) {
+                const int m = m0 + wm * TM + i * MI + rl;
+                if (m >= M) continue;
+                const size_t ro = static_cast<size_t>(m) * N + nj;
+                f32x4 rv[NQ];
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) rv[q] = *reinterpret_cast<const f32x4*>(res.x + ro + 8 * q);
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    f32x4 v;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+                    f32x4 h = rv[q];
+                    if constexpr (kResLn<EPI>) {
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) h[c] = fmaf((h[c] - stv[i].x) * stv[i].y, gj[q][c], ej[q][c]);
+                    }
+                    v += bj[q];
+                    v += h;
+                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + ro + 8 * q) = v;
+                }
+            }
+            // Keep the next block column's loads from being hoisted here: registers stay
+            // bounded by one block column's operands.
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
+        f32x4 bv[FN][NQ];
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int q = 0; q < NQ; ++q)
+                bv[j][q] = *reinterpret_cast<const f32x4*>(bias + n0 + wn * TN + j * MI + 8 * q + 4 * kg);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int m = m0 + wm * TM + i * MI + rl;
+            if (m >= M) continue;
+            const size_t ro = static_cast<size_t>(m) * N + n0 + wn * TN + 4 * kg;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+#pragma unroll
+                for (int q = 0; q < NQ; ++q) {
+                    f32x4 v;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
+                    v += bv[j][q];
                     if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
 #pragma unroll
                         for (int c = 0; c < 4; ++c) v[c] = gelu_erf(v[c]);
@@ -421,7 +479,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
                     u32x2 pk;
                     pk[0] = pack_bf16x2(v[0], v[1]);
                     pk[1] = pack_bf16x2(v[2], v[3]);
-                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + o) = pk;
+                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + ro + j * MI + 8 * q) = pk;
                 }
             }
         }
@@ -429,7 +487,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t
 }
 
 template <int BM, int BN, int WM, int WN, int MI, int S, int BK = 64>
-hipError_t launch_dlds(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
+hipError_t launch_dlds(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
                        int k, int epi, void* out, hipStream_t st, int group_m) {
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
@@ -445,8 +503,12 @@ hipError_t launch_dlds(const uint16_t* x, const uint16_t* w, const float* bias, 
             hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_RES_F32, BK>), grid, block, 0, st,
                                x, w, bias, res, out, m, n, k, group_m);
             break;
-        case kEpiResF32Ffn2:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResF32Ffn2, BK>), grid, block, 0, st, x, w,
+        case kEpiResLn:
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLn, BK>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k, group_m);
+            break;
+        case kEpiResLnFfn2:
+            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLnFfn2, BK>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         default:
@@ -489,7 +551,7 @@ __device__ __forceinline__ void interleave_step() {
 template <int BM, int BN, int WM, int WN, int MI, int EPI, int BK = 64, int OCC = 1, int S = 2>
 __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void gemm_sched_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, const float* __restrict__ bias,
-    const float* __restrict__ res, void* __restrict__ out, int M, int N, int K, int group_m) {
+    Residual res, void* __restrict__ out, int M, int N, int K, int group_m) {
     typedef Mfma<MI> MF;
     typedef typename MF::acc_t acc_t;
     constexpr int NW = WM * WN;
@@ -620,7 +682,7 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(O
     // activation / residual applied), then writes it back as whole rows, 16 bytes per lane,
     // so every store instruction covers full cache lines.
     static_assert(MI == 32, "staged epilogue assumes 32-row MFMA blocks");
-    constexpr bool F32OUT = (EPI == ELIS_EPI_BIAS_RES_F32 || EPI == kEpiResF32Ffn2);
+    constexpr bool F32OUT = kF32Out<EPI>;
     constexpr int EB = F32OUT ? 4 : 2;          // output element bytes
     constexpr int ROWB = TN * EB;               // bytes of one wave-tile row
     constexpr int PITCH = ROWB + 16;            // padded LDS row pitch
@@ -629,6 +691,14 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(O
     static_assert(NW * 32 * PITCH <= S * STAGE * 2, "staging must fit in the stage buffers");
     block_sync_lds();  // every wave is done with the stage buffers
     char* stg = reinterpret_cast<char*>(smem) + wid * 32 * PITCH;
+    // On read-back a lane always covers the same 16 output bytes of a row: columns nl ...
+    const int ch = lane % LPR;
+    const int nl = n0 + wn * TN + ch * (16 / EB);
+    f32x4 gl, bl;  // LayerNorm g, b of those columns (LayerNorm-form residual)
+    if constexpr (kResLn<EPI>) {
+        gl = *reinterpret_cast<const f32x4*>(res.g + nl);
+        bl = *reinterpret_cast<const f32x4*>(res.b + nl);
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -657,19 +727,40 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(O
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         __builtin_amdgcn_wave_barrier();
         asm volatile("" ::: "memory");
+        constexpr int NRR = 32 / RPR;  // read-back rows per lane per block row
+        if constexpr (F32OUT) {
+            // All residual vectors (and row statistics) of the block row are requested first.
+            f32x4 hv[NRR];
+            float2 sv[NRR];
 #pragma unroll
-        for (int rr = 0; rr < 32 / RPR; ++rr) {
-            const int row = rr * RPR + lane / LPR, ch = lane % LPR;
-            const int m = m0 + wm * TM + i * MI + row;
-            const u32x4 d = *reinterpret_cast<const u32x4*>(stg + row * PITCH + ch * 16);
-            if (m < M) {
-                const size_t o = static_cast<size_t>(m) * N + n0 + wn * TN + ch * (16 / EB);
-                if constexpr (F32OUT) {
-                    f32x4 v = __builtin_bit_cast(f32x4, d) + *reinterpret_cast<const f32x4*>(res + o);
-                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + o) = v;
-                } else {
-                    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(out) + o) = d;
+            for (int rr = 0; rr < NRR; ++rr) {
+                const int m = m0 + wm * TM + i * MI + rr * RPR + lane / LPR;
+                const int mc = m < M ? m : M - 1;  // rows past the end load a valid row, store nothing
+                hv[rr] = *reinterpret_cast<const f32x4*>(res.x + static_cast<size_t>(mc) * N + nl);
+                if constexpr (kResLn<EPI>) sv[rr] = res.stats[mc];
+            }
+#pragma unroll
+            for (int rr = 0; rr < NRR; ++rr) {
+                const int row = rr * RPR + lane / LPR;
+                const int m = m0 + wm * TM + i * MI + row;
+                const u32x4 d = *reinterpret_cast<const u32x4*>(stg + row * PITCH + ch * 16);
+                if (m < M) {
+                    f32x4 h = hv[rr];
+                    if constexpr (kResLn<EPI>) {
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) h[c] = fmaf((h[c] - sv[rr].x) * sv[rr].y, gl[c], bl[c]);
+                    }
+                    const f32x4 v = __builtin_bit_cast(f32x4, d) + h;
+                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + static_cast<size_t>(m) * N + nl) = v;
                 }
+            }
+        } else {
+#pragma unroll
+            for (int rr = 0; rr < NRR; ++rr) {
+                const int row = rr * RPR + lane / LPR;
+                const int m = m0 + wm * TM + i * MI + row;
+                const u32x4 d = *reinterpret_cast<const u32x4*>(stg + row * PITCH + ch * 16);
+                if (m < M) *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(out) + static_cast<size_t>(m) * N + nl) = d;
             }
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -679,7 +770,7 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(O
 }
 
 template <int BM, int BN, int WM, int WN, int MI, int BK = 64, int OCC = 1, int S = 2>
-hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
+hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
                         int k, int epi, void* out, hipStream_t st, int group_m) {
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
@@ -695,8 +786,12 @@ hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias,
             hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, BK, OCC, S>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
-        case kEpiResF32Ffn2:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResF32Ffn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+        case kEpiResLn:
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLn, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+                               out, m, n, k, group_m);
+            break;
+        case kEpiResLnFfn2:
+            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
                                out, m, n, k, group_m);
             break;
         default:
@@ -706,7 +801,7 @@ hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias,
 }
 
 template <int BM, int BN, int WM, int WN, int MI>
-hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
+hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
                        int k, int epi, void* out, hipStream_t st) {
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
@@ -722,8 +817,12 @@ hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, 
             hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k);
             break;
-        case kEpiResF32Ffn2:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, kEpiResF32Ffn2>), grid, block, 0, st, x, w, bias,
+        case kEpiResLn:
+            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLn>), grid, block, 0, st, x, w, bias,
+                               res, out, m, n, k);
+            break;
+        case kEpiResLnFfn2:
+            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2>), grid, block, 0, st, x, w, bias,
                                res, out, m, n, k);
             break;
         default:
@@ -736,13 +835,14 @@ hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, 
 
 // Tile configurations (ids are internal; benchmarks sweep them).
 hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uint16_t* w, const float* bias,
-                              const float* res, int m, int n, int k, int epi, void* out, hipStream_t st) {
+                              Residual res, int m, int n, int k, int epi, void* out, hipStream_t st) {
     switch (cfg) {
         case 0: return launch_tile<128, 128, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
         case 1: return launch_tile<128, 64, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
         case 14: return launch_dlds<256, 256, 2, 4, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 19: return launch_dlds<128, 128, 2, 2, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 21: return launch_sched<256, 256, 2, 4, 32>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 32: return launch_sched<128, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         default: return hipErrorInvalidValue;
     }
 }
@@ -761,16 +861,16 @@ int gemm_config_bn(int cfg) {
 //   bf16 out, bias + GELU (FFN1):    8-wave 256 x 256 direct-to-LDS
 //   fp32 out, bias + residual:       4-wave 128 x 128 direct-to-LDS; the 8-wave 256 x 256
 //                                    one when K is long and M large (FFN2 at >= 48K tokens)
-hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m, int n,
-                       int k, int epi, void* out, hipStream_t st, bool ffn2) {
-    if (ffn2 && epi == ELIS_EPI_BIAS_RES_F32) epi = kEpiResF32Ffn2;
+hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
+                       int k, int epi, void* out, hipStream_t st) {
     if (m < 1 || n % 64 != 0 || k % kBK != 0 || n < 64 || k < kBK) return hipErrorInvalidValue;
     constexpr int kGroupM = 8;
     const bool n256 = n % 256 == 0, n128 = n % 128 == 0;
     int cfg = n128 ? 19 : 1;
     if (epi == ELIS_EPI_BIAS_BF16 && n256) cfg = 21;
     else if (epi == ELIS_EPI_BIAS_GELU_BF16 && n256) cfg = 14;
-    else if ((epi == ELIS_EPI_BIAS_RES_F32 || epi == kEpiResF32Ffn2) && n256 && k >= 2048 && m >= 49152) cfg = 14;
+    else if ((epi == ELIS_EPI_BIAS_RES_F32 || kResLnCode(epi)) && n256 && k >= 2048 && m >= 49152) cfg = 14;
+    else if (kResLnCode(epi) && n128) cfg = 32;
     return launch_gemm_config(cfg, cfg == 1 ? 1 : kGroupM, x, w, bias, res, m, n, k, epi, out, st);
 }
 

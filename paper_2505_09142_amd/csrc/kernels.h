@@ -11,20 +11,43 @@ hipError_t launch_seqmap(const int32_t* cu, int n, int total, int max_seqlen, Se
                          uint32_t* status, hipStream_t st);
 
 // norm.hip
+// Row outputs of a LayerNorm y = (z - mean) * rstd * g + b (any pointer may be null):
+//   y32   fp32 y;  y16  bf16 y;  z32  the pre-norm row z itself (embedding only);
+//   stats (mean, rstd) of the row, from which a later epilogue rebuilds y out of z.
+struct LnOut {
+    float* y32;
+    uint16_t* y16;
+    float* z32;
+    float2* stats;
+};
 hipError_t launch_embed_ln(const int32_t* ids, const int32_t* cu, int n, int total,
                            const uint16_t* word, const uint16_t* pos, const float* type0,
                            const float* g, const float* b, int d, int vocab, int max_pos, float eps,
-                           float* out32, uint16_t* out16, uint32_t* status, hipStream_t st);
+                           LnOut out, uint32_t* status, hipStream_t st);
 hipError_t launch_layernorm(const float* x, const float* g, const float* b, int rows, int d, float eps,
-                            float* out32, uint16_t* out16, hipStream_t st);
+                            LnOut out, hipStream_t st);
 
 // gemm.hip
-// ffn2 selects a separately named instantiation of the residual epilogue (profiling only).
-hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, const float* res, int m,
-                       int n, int k, int epi, void* out, hipStream_t st, bool ffn2 = false);
+// Residual added by the fp32-output epilogues: the fp32 matrix x itself (stats null), or the
+// LayerNorm output rebuilt from its pre-norm input x: fmaf((x - mean) * rstd, g, b), the same
+// expression the LayerNorm kernel evaluates, so both see bit-identical values.
+struct Residual {
+    const float* x;       // [M, N]
+    const float2* stats;  // [M] (mean, rstd), or null
+    const float* g;       // [N]
+    const float* b;       // [N]
+};
+// Internal epilogue codes beyond the public ELIS_EPI_*: fp32 output + bias + LayerNorm-form
+// residual. Same arithmetic; two instantiations so that the attention output projection and
+// the second feed-forward product carry their own kernel names in profiles.
+constexpr int kEpiResLn = 4;
+constexpr int kEpiResLnFfn2 = 5;
+
+hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
+                       int k, int epi, void* out, hipStream_t st);
 
 hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uint16_t* w, const float* bias,
-                              const float* res, int m, int n, int k, int epi, void* out, hipStream_t st);
+                              Residual res, int m, int n, int k, int epi, void* out, hipStream_t st);
 int gemm_config_bn(int cfg);
 
 // attention.hip

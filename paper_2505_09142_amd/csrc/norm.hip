@@ -5,6 +5,11 @@
 // so a wave reads a row in fully coalesced 1 KiB sweeps. Mean and variance are
 // two-pass over the registers (no E[x^2] - E[x]^2 cancellation), reduced with
 // cross-lane shuffles.
+//
+// Outputs (LnOut): the fp32 and/or bf16 normalised row, and optionally the row
+// statistics (mean, rstd) instead of an fp32 copy: the fp32-output GEMM that
+// consumes the row as its residual rebuilds y = fmaf((z - mean) * rstd, g, b)
+// from the pre-norm row z, which saves writing and re-reading an fp32 copy.
 #include "kernels.h"
 
 namespace elis {
@@ -15,8 +20,9 @@ constexpr int kRowsPerBlock = 4;  // 4 waves, one row each
 
 template <int VPL>
 __device__ __forceinline__ void ln_finish(f32x4 (&v)[VPL], int lane, int d, const float* __restrict__ g,
-                                          const float* __restrict__ b, float eps, float* __restrict__ o32,
-                                          uint16_t* __restrict__ o16) {
+                                          const float* __restrict__ b, float eps, size_t row, const LnOut& o) {
+    float* o32 = o.y32 ? o.y32 + row * d : nullptr;
+    uint16_t* o16 = o.y16 ? o.y16 + row * d : nullptr;
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
@@ -39,6 +45,7 @@ __device__ __forceinline__ void ln_finish(f32x4 (&v)[VPL], int lane, int d, cons
     }
     const float var = wave_sum(q) * inv_d;
     const float rstd = 1.0f / sqrtf(var + eps);
+    if (o.stats && lane == 0) o.stats[row] = make_float2(mean, rstd);
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
         const int e = 4 * (lane + kWave * i);
@@ -47,7 +54,7 @@ __device__ __forceinline__ void ln_finish(f32x4 (&v)[VPL], int lane, int d, cons
             const f32x4 bv = *reinterpret_cast<const f32x4*>(b + e);
             f32x4 y;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) y[c] = (v[i][c] - mean) * rstd * gv[c] + bv[c];
+            for (int c = 0; c < 4; ++c) y[c] = fmaf((v[i][c] - mean) * rstd, gv[c], bv[c]);
             if (o32) *reinterpret_cast<f32x4*>(o32 + e) = y;
             if (o16) {
                 u32x2 p;
@@ -74,7 +81,7 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void embed_ln_kernel(
     const int32_t* __restrict__ ids, const int32_t* __restrict__ cu, int n, int total,
     const uint16_t* __restrict__ word, const uint16_t* __restrict__ pos, const float* __restrict__ type0,
     const float* __restrict__ g, const float* __restrict__ b, int d, int vocab, int max_pos, float eps,
-    float* __restrict__ out32, uint16_t* __restrict__ out16, uint32_t* __restrict__ status) {
+    LnOut out, uint32_t* __restrict__ status) {
     const int lane = threadIdx.x & (kWave - 1);
     const int t = blockIdx.x * kRowsPerBlock + (threadIdx.x / kWave);
     if (t >= total) return;
@@ -92,18 +99,19 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void embed_ln_kernel(
 #pragma unroll
     for (int i = 0; i < VPL; ++i) {
         const int e = 4 * (lane + kWave * i);
-        if (e < d) v[i] = load_bf16x4(wr + e) + load_bf16x4(pr + e) + *reinterpret_cast<const f32x4*>(type0 + e);
+        if (e < d) {
+            v[i] = load_bf16x4(wr + e) + load_bf16x4(pr + e) + *reinterpret_cast<const f32x4*>(type0 + e);
+            if (out.z32) *reinterpret_cast<f32x4*>(out.z32 + static_cast<size_t>(t) * d + e) = v[i];
+        }
     }
-    const size_t off = static_cast<size_t>(t) * d;
-    ln_finish<VPL>(v, lane, d, g, b, eps, out32 ? out32 + off : nullptr, out16 ? out16 + off : nullptr);
+    ln_finish<VPL>(v, lane, d, g, b, eps, static_cast<size_t>(t), out);
 }
 
 template <int VPL>
 __global__ __launch_bounds__(kRowsPerBlock* kWave) void layernorm_kernel(const float* __restrict__ x,
                                                                          const float* __restrict__ g,
                                                                          const float* __restrict__ b, int rows,
-                                                                         int d, float eps, float* __restrict__ o32,
-                                                                         uint16_t* __restrict__ o16) {
+                                                                         int d, float eps, LnOut out) {
     const int lane = threadIdx.x & (kWave - 1);
     const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x / kWave);
     if (r >= rows) return;
@@ -114,7 +122,7 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void layernorm_kernel(const f
         const int e = 4 * (lane + kWave * i);
         if (e < d) v[i] = *reinterpret_cast<const f32x4*>(x + off + e);
     }
-    ln_finish<VPL>(v, lane, d, g, b, eps, o32 ? o32 + off : nullptr, o16 ? o16 + off : nullptr);
+    ln_finish<VPL>(v, lane, d, g, b, eps, static_cast<size_t>(r), out);
 }
 
 }  // namespace
@@ -134,21 +142,20 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void layernorm_kernel(const f
 
 hipError_t launch_embed_ln(const int32_t* ids, const int32_t* cu, int n, int total, const uint16_t* word,
                            const uint16_t* pos, const float* type0, const float* g, const float* b, int d,
-                           int vocab, int max_pos, float eps, float* out32, uint16_t* out16, uint32_t* status,
-                           hipStream_t st) {
+                           int vocab, int max_pos, float eps, LnOut out, uint32_t* status, hipStream_t st) {
     const dim3 grid((total + kRowsPerBlock - 1) / kRowsPerBlock), block(kRowsPerBlock * kWave);
 #define CALL(V)                                                                                          \
     hipLaunchKernelGGL(embed_ln_kernel<V>, grid, block, 0, st, ids, cu, n, total, word, pos, type0, g, b, d, \
-                       vocab, max_pos, eps, out32, out16, status)
+                       vocab, max_pos, eps, out, status)
     ELIS_VPL_SWITCH(d, CALL)
 #undef CALL
     return hipGetLastError();
 }
 
 hipError_t launch_layernorm(const float* x, const float* g, const float* b, int rows, int d, float eps,
-                            float* out32, uint16_t* out16, hipStream_t st) {
+                            LnOut out, hipStream_t st) {
     const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock), block(kRowsPerBlock * kWave);
-#define CALL(V) hipLaunchKernelGGL(layernorm_kernel<V>, grid, block, 0, st, x, g, b, rows, d, eps, out32, out16)
+#define CALL(V) hipLaunchKernelGGL(layernorm_kernel<V>, grid, block, 0, st, x, g, b, rows, d, eps, out)
     ELIS_VPL_SWITCH(d, CALL)
 #undef CALL
     return hipGetLastError();
