@@ -203,6 +203,49 @@ def summarize_trace(stats_csv, command, bench_json):
     print(f"wrote {TRACE_PROFILE}")
 
 
+SELECT_PROFILE = os.path.join(ROOT, "profiles", "select_large_n.md")
+_SELECT_STAGES = ["init", "count 11b", "reduce", "count 11b", "reduce", "count 10b", "reduce", "scatter", "final"]
+
+
+def summarize_select(sweep_json, trace_csv, command):
+    """Write the large-n select summary: bench.py --select-sweep's line plus per-kernel medians
+    from a rocprofv3 kernel trace of the same command (each call is 9 launches in order)."""
+    import csv
+    import statistics
+    rows = json.loads(open(sweep_json).read().strip().splitlines()[-1])["select_sweep"]
+    with open(trace_csv) as f:
+        tr = sorted((r for r in csv.DictReader(f) if "select_" in r["Kernel_Name"]),
+                    key=lambda r: int(r["Start_Timestamp"]))
+    nk = len(_SELECT_STAGES)
+    calls = [tr[i:i + nk] for i in range(0, len(tr), nk)]
+    per_cfg = len(calls) // len(rows)
+    lines = ["# ISRTF select above 8192 jobs: device-wide radix selection, n = 2^20 .. 2^24", "",
+             "Commands (GPU box, repo root as working tree):", "",
+             "    python bench.py --select-sweep", f"    {command}", "",
+             "Predictions 250 + 100 * N(0, 0.55^2) (the predictor's output scale), arrivals a random "
+             "permutation. `mandatory` = 12 n bytes in (pred + arrival) + 4 k out; HBM fraction = "
+             "mandatory bytes / time / 8 TB/s. The implementation reads pred four times (16 n bytes) "
+             "and arrivals only for jobs tied on the prediction.", "",
+             "| n | k | µs per call (HIP events) | GB/s of mandatory bytes | HBM fraction |",
+             "|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        lines.append(f"| 2^{r['n'].bit_length() - 1} | {r['k']} | {r['us']:.1f} | {r['gbs']:.0f} | {r['hbm_frac']:.3f} |")
+    lines += ["", "Per-kernel medians from the trace (µs; a stage that finds its bucket already resolved "
+              "returns at once):", "",
+              "| n | k | " + " | ".join(_SELECT_STAGES) + " |", "|---:|---:|" + "---:|" * nk]
+    for ci, r in enumerate(rows):
+        cs = calls[ci * per_cfg + 3:(ci + 1) * per_cfg]
+        med = [statistics.median((int(c[j]["End_Timestamp"]) - int(c[j]["Start_Timestamp"])) / 1e3 for c in cs)
+               for j in range(nk)]
+        lines.append(f"| 2^{r['n'].bit_length() - 1} | {r['k']} | " + " | ".join(f"{v:.1f}" for v in med) + " |")
+    lines += ["", "Small launches cost 2-5 µs each (nine per call), so below 2^22 jobs the call is "
+              "launch-bound; at k = 8192 the one-work-group bitonic sort of the chosen jobs (~170 µs) "
+              "dominates."]
+    with open(SELECT_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {SELECT_PROFILE}")
+
+
 def cpu_baseline(w, W, b, seconds: float):
     import numpy as np
     import threadpoolctl
@@ -224,6 +267,56 @@ def cpu_baseline(w, W, b, seconds: float):
             "tokens_per_s": toks / el, "host_cpus": len(os.sched_getaffinity(0))}
 
 
+def select_sweep(ks=(64, 8192), iters=20):
+    """Device-wide ISRTF select at n = 2^20 .. 2^24: time per call and its HBM fraction.
+
+    Predictions are drawn like the predictor's outputs (250 + 100 * N(0, 0.55^2)),
+    arrivals are a random permutation. Mandatory bytes = 12 n in (pred + arrival)
+    + 4 k out; the implementation reads pred four times (16 n) and arrivals for ties only."""
+    import numpy as np
+    import torch
+
+    from paper_2505_09142_amd import _elis as E
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    rows = []
+    for lg in range(20, 25):
+        n = 1 << lg
+        rng = np.random.default_rng(lg)
+        pred = torch.from_numpy((250.0 + 100.0 * 0.55 * rng.standard_normal(n)).astype(np.float32)).to(dev)
+        arr = torch.from_numpy(rng.permutation(n).astype(np.int64)).to(dev)
+        wsb = E.elis_select_workspace_bytes(n)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        for k in ks:
+            idx = torch.empty(k, dtype=torch.int32, device=dev)
+            cnt = torch.empty(1, dtype=torch.int32, device=dev)
+
+            def call():
+                E.check(E.elis_isrtf_select(pred.data_ptr(), arr.data_ptr(), n, k, idx.data_ptr(), cnt.data_ptr(),
+                                            ws.data_ptr(), wsb, stream), "select")
+            for _ in range(3):
+                call()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(iters):
+                call()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / iters * 1e3
+            mand = 12.0 * n + 4.0 * k
+            rows.append({"n": n, "k": k, "us": us, "mandatory_bytes": mand,
+                         "gbs": mand / us / 1e3, "hbm_frac": mand / us / 1e3 / PEAK_HBM_GBS,
+                         "read_bytes": 16.0 * n})
+            print(f"select n=2^{lg} k={k}: {us:.1f} us, {mand / us / 1e3:.0f} GB/s of mandatory bytes", file=sys.stderr,
+                  flush=True)
+    st, bits = E.elis_read_status(ws.data_ptr(), stream)
+    if st != E.ELIS_OK:
+        raise SystemExit(f"device status {st} bits {bits}")
+    print(json.dumps({"select_sweep": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -237,11 +330,21 @@ def main():
                          "(reference dispatches for PMC byte counters)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the HBM-traffic summary from two rocprofv3 --pmc counter_collection.csv files")
+    ap.add_argument("--select-sweep", action="store_true",
+                    help="time the device-wide select at n = 2^20 .. 2^24 instead of the step")
+    ap.add_argument("--summarize-select", nargs=3, metavar=("SWEEP_JSON", "TRACE_CSV", "COMMAND"),
+                    help="write the large-n select summary")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("STATS_CSV", "BENCH_JSON", "COMMAND"),
                     help="write the kernel-trace summary from a rocprofv3 kernel_stats.csv")
     ap.add_argument("--pmc-command", action="append", default=[],
                     help="with --summarize-pmc: the command of each pass, recorded in the summary")
     args = ap.parse_args()
+    if args.summarize_select:
+        summarize_select(*args.summarize_select)
+        return
+    if args.select_sweep:
+        select_sweep()
+        return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace[0], args.summarize_trace[2], args.summarize_trace[1])
         return

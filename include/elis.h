@@ -122,10 +122,22 @@ int elis_predict_remaining(const elis_weights *w, const int32_t *token_ids,
                            int32_t max_seqlen, float *out_pred, float *out_hidden,
                            void *workspace, size_t ws_bytes, void *stream);
 
-/* Largest n accepted by elis_isrtf_select in this build. */
+/* Largest n accepted by elis_isrtf_select in this build (2^28). */
 int32_t elis_select_max_n(void);
 
-/* Bytes of device workspace elis_isrtf_select needs for n jobs (0 if n invalid). */
+/*
+ * Largest min(batch_cap, n) accepted for n jobs (0 if n is invalid): unbounded
+ * (INT32_MAX) for n <= 8192, where one work-group sorts every job; 8192 above,
+ * where the chosen jobs are sorted by one work-group after a device-wide radix
+ * selection.
+ */
+int32_t elis_select_max_batch_cap(int32_t n);
+
+/*
+ * Bytes of device workspace elis_isrtf_select needs for n jobs (0 if n is
+ * invalid): 256 for n <= 8192, about 4n + 41 KiB above (a tie list of up to n
+ * indices plus counters and a 2048-bin histogram).
+ */
 size_t elis_select_workspace_bytes(int32_t n);
 
 /*
@@ -138,7 +150,10 @@ size_t elis_select_workspace_bytes(int32_t n);
  *  pred        fp32 [n], arrival_seq int64 [n]
  *  out_idx     int32 [batch_cap] (only the first min(batch_cap, n) are written)
  *  out_count   int32 [1] device: set to min(batch_cap, n)
- * batch_cap == 0 is valid (count 0). 1 <= n <= elis_select_max_n().
+ * batch_cap == 0 is valid (count 0). 1 <= n <= elis_select_max_n() (else
+ * ELIS_ESHAPE); min(batch_cap, n) <= elis_select_max_batch_cap(n) (else
+ * ELIS_EUNSUPPORTED). Enqueue only; out_idx / out_count are valid once the
+ * stream reaches the call.
  */
 int elis_isrtf_select(const float *pred, const int64_t *arrival_seq, int32_t n,
                       int32_t batch_cap, int32_t *out_idx, int32_t *out_count,

@@ -73,6 +73,7 @@ SIGNATURES = {
     "elis_predict_remaining": (c_int, [POINTER(elis_weights), c_void_p, c_void_p, c_int32, c_int32, c_int32,
                                        c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "elis_select_max_n": (c_int32, []),
+    "elis_select_max_batch_cap": (c_int32, [c_int32]),
     "elis_select_workspace_bytes": (c_size_t, [c_int32]),
     "elis_isrtf_select": (c_int, [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_size_t,
                                   c_void_p]),
@@ -128,6 +129,10 @@ def elis_predict_remaining(w: elis_weights, token_ids: int, cu_seqlens: int, n_s
 
 def elis_select_max_n() -> int:
     return lib().elis_select_max_n()
+
+
+def elis_select_max_batch_cap(n: int) -> int:
+    return lib().elis_select_max_batch_cap(n)
 
 
 def elis_select_workspace_bytes(n: int) -> int:

@@ -256,10 +256,12 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
 
 int32_t elis_select_max_n(void) { return select_max_n(); }
 
-size_t elis_select_workspace_bytes(int32_t n) {
+int32_t elis_select_max_batch_cap(int32_t n) {
     if (n < 1 || n > select_max_n()) return 0;
-    return align_up(sizeof(uint32_t));
+    return select_max_k(n);
 }
+
+size_t elis_select_workspace_bytes(int32_t n) { return select_workspace_bytes(n); }
 
 int elis_isrtf_select(const float* pred, const int64_t* arrival_seq, int32_t n, int32_t batch_cap,
                       int32_t* out_idx, int32_t* out_count, void* workspace, size_t ws_bytes, void* stream) {
@@ -267,11 +269,11 @@ int elis_isrtf_select(const float* pred, const int64_t* arrival_seq, int32_t n, 
     if (n <= 0 || batch_cap < 0) return ELIS_EINVAL;
     if (!aligned(workspace)) return ELIS_EINVAL;
     if (n > select_max_n()) return ELIS_ESHAPE;
-    if (ws_bytes < elis_select_workspace_bytes(n)) return ELIS_EWORKSPACE;
+    if ((batch_cap < n ? batch_cap : n) > select_max_k(n)) return ELIS_EUNSUPPORTED;
+    if (ws_bytes < select_workspace_bytes(n)) return ELIS_EWORKSPACE;
     hipStream_t st = static_cast<hipStream_t>(stream);
     hipError_t e = timed(ELIS_K_SELECT, st, [&] {
-        return launch_select(pred, arrival_seq, n, batch_cap, out_idx, out_count, static_cast<uint32_t*>(workspace),
-                             st);
+        return launch_select(pred, arrival_seq, n, batch_cap, out_idx, out_count, workspace, st);
     });
     return status_of(e);
 }

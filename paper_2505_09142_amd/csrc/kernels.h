@@ -68,7 +68,10 @@ hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int
 
 // select.hip
 int select_max_n();
+int select_max_k(int n);  // largest batch cap accepted for n jobs
+size_t select_workspace_bytes(int n);
+// workspace: select_workspace_bytes(n) bytes, 256-byte aligned; its first word is the status.
 hipError_t launch_select(const float* pred, const int64_t* arrival, int n, int k, int32_t* out_idx,
-                         int32_t* out_count, uint32_t* status, hipStream_t st);
+                         int32_t* out_count, void* workspace, hipStream_t st);
 
 }  // namespace elis

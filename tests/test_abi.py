@@ -59,6 +59,14 @@ def test_workspace_queries(lib):
     assert E.elis_select_workspace_bytes(0) == 0
     assert E.elis_select_workspace_bytes(E.elis_select_max_n() + 1) == 0
     assert E.elis_select_workspace_bytes(64) >= 4
+    # above 8192 jobs: a tie list of up to n indices
+    assert E.elis_select_workspace_bytes(8193) >= 4 * 8193
+    assert E.elis_select_workspace_bytes(1 << 24) >= 4 * (1 << 24)
+    assert E.elis_select_max_n() == 1 << 28
+    assert E.elis_select_max_batch_cap(0) == 0
+    assert E.elis_select_max_batch_cap(8192) == 2 ** 31 - 1
+    assert E.elis_select_max_batch_cap(8193) == 8192
+    assert E.elis_select_max_batch_cap(E.elis_select_max_n() + 1) == 0
     assert E.elis_attention_workspace_bytes(4, 100) > 0
     assert E.elis_attention_workspace_bytes(4, 3) == 0
 
@@ -135,6 +143,10 @@ def test_select_rejects_invalid_arguments(lib):
     assert call(ws=FAKE_WS + 4) == E.ELIS_EINVAL
     assert call(n=E.elis_select_max_n() + 1) == E.ELIS_ESHAPE
     assert call(wsb=0) == E.ELIS_EWORKSPACE
+    # more than 8192 jobs: at most 8192 chosen
+    big = E.elis_select_workspace_bytes(100000)
+    assert call(n=100000, k=8193, wsb=big) == E.ELIS_EUNSUPPORTED
+    assert call(n=100000, k=8192, wsb=big - 1) == E.ELIS_EWORKSPACE
 
 
 def test_building_blocks_reject_invalid_arguments(lib):

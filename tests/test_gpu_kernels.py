@@ -77,6 +77,67 @@ def test_select_worked_example():
         assert idx.cpu().numpy()[:int(cnt.item())].tolist() == c["selected"]
 
 
+# ------------------------------------------------------------------------------ select, large n
+# Above 8192 jobs the device-wide radix selection runs; "ties" (four distinct values) and
+# "equal" give tie sets above 8192, which exercises the selection among ties by arrival.
+SELECT_LARGE_CASES = [(8193, "normal"), (8193, "equal"), (20000, "special"), (100003, "ties"),
+                      (100003, "normal"), (1 << 20, "normal"), (1 << 20, "special")]
+
+
+def _run_select(d_pred, d_arr, n, k, ws, wsb):
+    idx = torch.full((max(1, k),), -1, dtype=torch.int32, device="cuda")
+    cnt = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    ok(E.elis_isrtf_select(d_pred.data_ptr(), d_arr.data_ptr(), n, k, idx.data_ptr(), cnt.data_ptr(), ws, wsb,
+                           stream()), "select")
+    torch.cuda.synchronize()
+    assert int(cnt.item()) == min(k, n)
+    st, bits = E.elis_read_status(ws, stream())
+    assert st == E.ELIS_OK and bits == 0
+    return idx.cpu().numpy()[:min(k, n)]
+
+
+@pytest.mark.parametrize("n,kind", SELECT_LARGE_CASES)
+def test_select_large_bit_exact(n, kind):
+    rng = np.random.default_rng(n + 31 * len(kind))
+    pred = _preds(kind, n, rng)
+    arr = rng.integers(0, max(2, n // 2), size=n).astype(np.int64)
+    order = np.asarray(oracle.oracle_order(pred, arr), dtype=np.int32)
+    d_pred, d_arr = dev(pred), dev(arr)
+    buf, ws, wsb = workspace(E.elis_select_workspace_bytes(n))
+    for k in (0, 1, 37, 8192):
+        note(f"select large n={n} kind={kind} k={k}")
+        got = _run_select(d_pred, d_arr, n, k, ws, wsb)
+        assert np.array_equal(got, order[:min(k, n)]), f"n={n} kind={kind} k={k}"
+
+
+def _order_key_np(pred):
+    u = pred.view(np.uint32).copy()
+    u[u == 0x80000000] = 0
+    key = np.where(u & 0x80000000, ~u, u | 0x80000000).astype(np.uint32)
+    key[np.isnan(pred)] = 0xFFFFFFFF
+    return key
+
+
+@pytest.mark.parametrize("n,kind,k", [(1 << 24, "normal", 64), (1 << 24, "normal", 8192), (1 << 22, "ties", 500)])
+def test_select_large_properties(n, kind, k):
+    """At sizes the sort-based oracle does not reach: the output is strictly increasing in
+    the total order (key, arrival, index), and exactly k-1 jobs precede its last element."""
+    rng = np.random.default_rng(n + k)
+    pred = _preds(kind, n, rng)
+    arr = rng.integers(0, n, size=n).astype(np.int64)
+    note(f"select properties n={n} kind={kind} k={k}")
+    buf, ws, wsb = workspace(E.elis_select_workspace_bytes(n))
+    got = _run_select(dev(pred), dev(arr), n, k, ws, wsb)
+    key = _order_key_np(pred)
+    gk, ga = key[got].astype(np.int64), arr[got]
+    inc = (gk[1:] > gk[:-1]) | ((gk[1:] == gk[:-1]) & ((ga[1:] > ga[:-1]) | ((ga[1:] == ga[:-1]) & (got[1:] > got[:-1]))))
+    assert inc.all()
+    lk, la, li = int(gk[-1]), int(ga[-1]), int(got[-1])
+    idx = np.arange(n)
+    before = (key < lk) | ((key == lk) & ((arr < la) | ((arr == la) & (idx < li))))
+    assert int(before.sum()) == k - 1
+
+
 # ------------------------------------------------------------------------------ LayerNorm
 
 @pytest.mark.parametrize("rows,d", [(1, 64), (7, 128), (1000, 768), (333, 1024), (65, 2048)])
