@@ -49,6 +49,8 @@ extern "C" {
 #define ELIS_DEV_BAD_TOKEN   1u  /* a token id outside [0, vocab)                    */
 #define ELIS_DEV_BAD_CU      2u  /* cu_seqlens[0] != 0, not increasing, or != T at n */
 #define ELIS_DEV_LONG_SEQ    4u  /* a sequence longer than max_seqlen               */
+#define ELIS_DEV_BAD_SLOT    8u  /* a job-table slot outside [0, max_jobs), or a negative token count */
+#define ELIS_DEV_PACK_SIZE  16u  /* packed lengths disagree with the host's total / max, or a job is empty */
 
 /* ------------------------------------------------------------------ model */
 #define ELIS_POOL_CLS  0 /* the first token's final hidden vector (Sec. 3.2)              */
@@ -169,6 +171,71 @@ int elis_read_status(const void *workspace, void *stream, uint32_t *bits);
 /* Human-readable name of a status code (static string). */
 const char *elis_status_string(int status);
 
+/* ------------------------------------------------------------------ device-resident job table
+ * The input side of a scheduling round kept in HBM (Alg. 1: the Job Pool is
+ * re-predicted from prompt + generated tokens; unchanged jobs keep their
+ * prediction). A caller-allocated table of max_jobs slots holds, per job, its
+ * first token, a ring of its most recent max_pos - 1 tokens, its length, its
+ * last prediction and its arrival sequence number. A round appends only the
+ * new tokens, packs the re-score set into token_ids / cu_seqlens on the
+ * device (input = the job's tokens, or past max_pos tokens the first one plus
+ * the most recent max_pos - 1), stores the new predictions, and selects over
+ * the cached predictions of the active jobs. Same conventions as above: plain
+ * device pointers, enqueue only, errors returned; content errors (a slot
+ * outside [0, max_jobs), packed sizes that disagree with the host's) set
+ * ELIS_DEV_* bits in the table's status word (read it with elis_read_status
+ * on `base`). A call must not name one slot twice.
+ */
+typedef struct {
+    void *base;       /* device, 256-byte aligned, elis_jobs_table_bytes() bytes */
+    int32_t max_jobs; /* slots 0 .. max_jobs-1                                    */
+    int32_t max_pos;  /* the encoder's position table (>= 2)                      */
+} elis_job_table;
+
+/* Bytes of the table (0 if max_jobs < 1 or max_pos < 2). */
+size_t elis_jobs_table_bytes(int32_t max_jobs, int32_t max_pos);
+
+/* Every slot empty (length 0), status cleared. */
+int elis_jobs_init(const elis_job_table *t, void *stream);
+
+/* Start jobs: slot[i] becomes empty with arrival_seq[i] (device arrays of m). */
+int elis_jobs_start(const elis_job_table *t, const int32_t *slots, const int64_t *arrival_seq, int32_t m,
+                    void *stream);
+
+/*
+ * Append tokens: job slots[i] (device int32 [m]) gets tokens[tok_offsets[i] ..
+ * tok_offsets[i+1]) (device int32 [m+1] offsets, starting at 0; tokens device
+ * int32 [total_new], total_new = tok_offsets[m] passed by the host).
+ */
+int elis_jobs_append(const elis_job_table *t, const int32_t *slots, const int32_t *tok_offsets,
+                     const int32_t *tokens, int32_t m, int32_t total_new, void *stream);
+
+/*
+ * Pack the predictor input of jobs slots[0..n) back to back: out_token_ids
+ * (device int32 [total_tokens]) and out_cu_seqlens (device int32 [n+1]).
+ * total_tokens = sum of min(length, max_pos) and max_seqlen (>= every such
+ * length, <= max_pos) are host ints the caller keeps from its own bookkeeping;
+ * a mismatch sets ELIS_DEV_PACK_SIZE and the output is undefined.
+ */
+int elis_jobs_pack(const elis_job_table *t, const int32_t *slots, int32_t n, int32_t total_tokens,
+                   int32_t max_seqlen, int32_t *out_token_ids, int32_t *out_cu_seqlens, void *stream);
+
+/* Cache predictions: the prediction of job slots[i] becomes pred[i] (device, n). */
+int elis_jobs_store_pred(const elis_job_table *t, const int32_t *slots, const float *pred, int32_t n,
+                         void *stream);
+
+/* Bytes of workspace elis_jobs_select needs for a active jobs (0 if invalid). */
+size_t elis_jobs_select_workspace_bytes(int32_t a);
+
+/*
+ * ISRTF select over the cached predictions of the active jobs slots[0..a)
+ * (same order and ties as elis_isrtf_select): out_slots (device int32
+ * [batch_cap]) gets the chosen job slots, highest priority first, out_count
+ * (device int32 [1]) their number. Limits of elis_isrtf_select apply with n = a.
+ */
+int elis_jobs_select(const elis_job_table *t, const int32_t *slots, int32_t a, int32_t batch_cap,
+                     int32_t *out_slots, int32_t *out_count, void *workspace, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------ building blocks
  * The predictor's kernels, exposed one by one for per-kernel parity tests and
  * measurement. Same conventions as above.
@@ -230,7 +297,8 @@ int elis_layernorm(const float *x, const float *g, const float *b, int32_t rows,
 #define ELIS_K_GEMM_FFN2 7
 #define ELIS_K_POOL_HEAD 8
 #define ELIS_K_SELECT    9
-#define ELIS_K_COUNT     10
+#define ELIS_K_JOBS      10 /* job-table append / pack / store / gather */
+#define ELIS_K_COUNT     11
 
 int elis_timing_enable(uint32_t class_mask); /* bit c enables class c; 0 disables */
 int elis_timing_reset(void);

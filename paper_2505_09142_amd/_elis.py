@@ -25,6 +25,8 @@ ELIS_EUNSUPPORTED = -6
 ELIS_DEV_BAD_TOKEN = 1
 ELIS_DEV_BAD_CU = 2
 ELIS_DEV_LONG_SEQ = 4
+ELIS_DEV_BAD_SLOT = 8
+ELIS_DEV_PACK_SIZE = 16
 
 ELIS_POOL_CLS = 0
 ELIS_POOL_MEAN = 1
@@ -34,7 +36,7 @@ ELIS_EPI_BIAS_GELU_BF16 = 1
 ELIS_EPI_BIAS_RES_F32 = 2
 
 KERNEL_CLASSES = ("seqmap", "embed_ln", "gemm_qkv", "attention", "gemm_o", "layernorm", "gemm_ffn1",
-                  "gemm_ffn2", "pool_head", "select")
+                  "gemm_ffn2", "pool_head", "select", "jobs")
 K = {name: i for i, name in enumerate(KERNEL_CLASSES)}
 
 
@@ -65,6 +67,10 @@ class elis_weights(ctypes.Structure):
                 ("head_w1", c_void_p), ("head_b1", c_void_p), ("head_w2", c_void_p), ("head_b2", c_void_p)]
 
 
+class elis_job_table(ctypes.Structure):
+    _fields_ = [("base", c_void_p), ("max_jobs", c_int32), ("max_pos", c_int32)]
+
+
 # name -> (restype, argtypes); mirrors include/elis.h
 SIGNATURES = {
     "elis_abi_version": (c_int32, []),
@@ -85,6 +91,17 @@ SIGNATURES = {
                                c_size_t, c_void_p]),
     "elis_layernorm": (c_int, [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_float, c_void_p, c_void_p,
                                c_void_p]),
+    "elis_jobs_table_bytes": (c_size_t, [c_int32, c_int32]),
+    "elis_jobs_init": (c_int, [POINTER(elis_job_table), c_void_p]),
+    "elis_jobs_start": (c_int, [POINTER(elis_job_table), c_void_p, c_void_p, c_int32, c_void_p]),
+    "elis_jobs_append": (c_int, [POINTER(elis_job_table), c_void_p, c_void_p, c_void_p, c_int32, c_int32,
+                                 c_void_p]),
+    "elis_jobs_pack": (c_int, [POINTER(elis_job_table), c_void_p, c_int32, c_int32, c_int32, c_void_p, c_void_p,
+                               c_void_p]),
+    "elis_jobs_store_pred": (c_int, [POINTER(elis_job_table), c_void_p, c_void_p, c_int32, c_void_p]),
+    "elis_jobs_select_workspace_bytes": (c_size_t, [c_int32]),
+    "elis_jobs_select": (c_int, [POINTER(elis_job_table), c_void_p, c_int32, c_int32, c_void_p, c_void_p,
+                                 c_void_p, c_size_t, c_void_p]),
     "elis_timing_enable": (c_int, [c_uint32]),
     "elis_timing_reset": (c_int, []),
     "elis_timing_read": (c_int, [c_int32, POINTER(c_int32), POINTER(c_double)]),
@@ -169,6 +186,45 @@ def elis_attention(qkv: int, cu_seqlens: int, n_seqs: int, total_tokens: int, ma
 def elis_layernorm(x: int, g: int, b: int, rows: int, d: int, eps: float, out_f32: int | None,
                    out_bf16: int | None, stream: int | None) -> int:
     return lib().elis_layernorm(x, g, b, rows, d, eps, out_f32, out_bf16, stream)
+
+
+def _tab(t):
+    return ctypes.byref(t) if t is not None else None
+
+
+def elis_jobs_table_bytes(max_jobs: int, max_pos: int) -> int:
+    return lib().elis_jobs_table_bytes(max_jobs, max_pos)
+
+
+def elis_jobs_init(t: elis_job_table, stream: int | None) -> int:
+    return lib().elis_jobs_init(_tab(t), stream)
+
+
+def elis_jobs_start(t: elis_job_table, slots: int, arrival_seq: int, m: int, stream: int | None) -> int:
+    return lib().elis_jobs_start(_tab(t), slots, arrival_seq, m, stream)
+
+
+def elis_jobs_append(t: elis_job_table, slots: int, tok_offsets: int, tokens: int | None, m: int, total_new: int,
+                     stream: int | None) -> int:
+    return lib().elis_jobs_append(_tab(t), slots, tok_offsets, tokens, m, total_new, stream)
+
+
+def elis_jobs_pack(t: elis_job_table, slots: int, n: int, total_tokens: int, max_seqlen: int, out_token_ids: int,
+                   out_cu_seqlens: int, stream: int | None) -> int:
+    return lib().elis_jobs_pack(_tab(t), slots, n, total_tokens, max_seqlen, out_token_ids, out_cu_seqlens, stream)
+
+
+def elis_jobs_store_pred(t: elis_job_table, slots: int, pred: int, n: int, stream: int | None) -> int:
+    return lib().elis_jobs_store_pred(_tab(t), slots, pred, n, stream)
+
+
+def elis_jobs_select_workspace_bytes(a: int) -> int:
+    return lib().elis_jobs_select_workspace_bytes(a)
+
+
+def elis_jobs_select(t: elis_job_table, slots: int, a: int, batch_cap: int, out_slots: int | None, out_count: int,
+                     workspace: int, ws_bytes: int, stream: int | None) -> int:
+    return lib().elis_jobs_select(_tab(t), slots, a, batch_cap, out_slots, out_count, workspace, ws_bytes, stream)
 
 
 def elis_timing_enable(class_mask: int) -> int:

@@ -278,6 +278,102 @@ int elis_isrtf_select(const float* pred, const int64_t* arrival_seq, int32_t n, 
     return status_of(e);
 }
 
+namespace {
+
+int check_table(const elis_job_table* t) {
+    if (!t || !t->base || t->max_jobs < 1 || t->max_pos < 2) return ELIS_EINVAL;
+    if (!aligned(t->base)) return ELIS_EINVAL;
+    return ELIS_OK;
+}
+
+}  // namespace
+
+size_t elis_jobs_table_bytes(int32_t max_jobs, int32_t max_pos) {
+    if (max_jobs < 1 || max_pos < 2) return 0;
+    return jobs_table_bytes(max_jobs, max_pos);
+}
+
+int elis_jobs_init(const elis_job_table* t, void* stream) {
+    int r = check_table(t);
+    if (r != ELIS_OK) return r;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return status_of(timed(ELIS_K_JOBS, st,
+                           [&] { return launch_jobs_init(jobs_table(t->base, t->max_jobs, t->max_pos), st); }));
+}
+
+int elis_jobs_start(const elis_job_table* t, const int32_t* slots, const int64_t* arrival_seq, int32_t m,
+                    void* stream) {
+    int r = check_table(t);
+    if (r != ELIS_OK) return r;
+    if (m < 0 || (m > 0 && (!slots || !arrival_seq))) return ELIS_EINVAL;
+    if (m == 0) return ELIS_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return status_of(timed(ELIS_K_JOBS, st, [&] {
+        return launch_jobs_start(jobs_table(t->base, t->max_jobs, t->max_pos), slots, arrival_seq, m, st);
+    }));
+}
+
+int elis_jobs_append(const elis_job_table* t, const int32_t* slots, const int32_t* tok_offsets,
+                     const int32_t* tokens, int32_t m, int32_t total_new, void* stream) {
+    int r = check_table(t);
+    if (r != ELIS_OK) return r;
+    if (m < 0 || total_new < 0) return ELIS_EINVAL;
+    if (m == 0) return ELIS_OK;
+    if (!slots || !tok_offsets || (total_new > 0 && !tokens)) return ELIS_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return status_of(timed(ELIS_K_JOBS, st, [&] {
+        return launch_jobs_append(jobs_table(t->base, t->max_jobs, t->max_pos), slots, tok_offsets, tokens, m,
+                                  total_new, st);
+    }));
+}
+
+int elis_jobs_pack(const elis_job_table* t, const int32_t* slots, int32_t n, int32_t total_tokens,
+                   int32_t max_seqlen, int32_t* out_token_ids, int32_t* out_cu_seqlens, void* stream) {
+    int r = check_table(t);
+    if (r != ELIS_OK) return r;
+    if (!slots || !out_token_ids || !out_cu_seqlens || n <= 0) return ELIS_EINVAL;
+    if (total_tokens < n || max_seqlen < 1 || max_seqlen > t->max_pos) return ELIS_ESHAPE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return status_of(timed(ELIS_K_JOBS, st, [&] {
+        return launch_jobs_pack(jobs_table(t->base, t->max_jobs, t->max_pos), slots, n, total_tokens, max_seqlen,
+                                out_token_ids, out_cu_seqlens, st);
+    }));
+}
+
+int elis_jobs_store_pred(const elis_job_table* t, const int32_t* slots, const float* pred, int32_t n,
+                         void* stream) {
+    int r = check_table(t);
+    if (r != ELIS_OK) return r;
+    if (n < 0 || (n > 0 && (!slots || !pred))) return ELIS_EINVAL;
+    if (n == 0) return ELIS_OK;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return status_of(timed(ELIS_K_JOBS, st, [&] {
+        return launch_jobs_store_pred(jobs_table(t->base, t->max_jobs, t->max_pos), slots, pred, n, st);
+    }));
+}
+
+size_t elis_jobs_select_workspace_bytes(int32_t a) {
+    if (a < 1 || a > select_max_n()) return 0;
+    return jobs_select_workspace_bytes(a);
+}
+
+int elis_jobs_select(const elis_job_table* t, const int32_t* slots, int32_t a, int32_t batch_cap,
+                     int32_t* out_slots, int32_t* out_count, void* workspace, size_t ws_bytes, void* stream) {
+    int r = check_table(t);
+    if (r != ELIS_OK) return r;
+    if (!slots || !out_count || !workspace || (batch_cap > 0 && !out_slots)) return ELIS_EINVAL;
+    if (a <= 0 || batch_cap < 0) return ELIS_EINVAL;
+    if (!aligned(workspace)) return ELIS_EINVAL;
+    if (a > select_max_n()) return ELIS_ESHAPE;
+    if ((batch_cap < a ? batch_cap : a) > select_max_k(a)) return ELIS_EUNSUPPORTED;
+    if (ws_bytes < jobs_select_workspace_bytes(a)) return ELIS_EWORKSPACE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    return status_of(timed(ELIS_K_SELECT, st, [&] {
+        return launch_jobs_select(jobs_table(t->base, t->max_jobs, t->max_pos), slots, a, batch_cap, out_slots,
+                                  out_count, workspace, st);
+    }));
+}
+
 int elis_read_status(const void* workspace, void* stream, uint32_t* bits) {
     if (!workspace) return ELIS_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);

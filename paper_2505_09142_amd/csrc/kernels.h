@@ -74,4 +74,28 @@ size_t select_workspace_bytes(int n);
 hipError_t launch_select(const float* pred, const int64_t* arrival, int n, int k, int32_t* out_idx,
                          int32_t* out_count, void* workspace, hipStream_t st);
 
+// jobs.hip: device-resident job table (first token, ring of the last max_pos - 1 tokens,
+// length, cached prediction, arrival) for incremental packing across rounds.
+struct JobTable {
+    uint32_t* status;
+    int32_t* first;    // [J]
+    int32_t* len;      // [J]
+    float* pred;       // [J]
+    int64_t* arrival;  // [J]
+    int32_t* ring;     // [J][max_pos - 1]
+    int max_jobs, max_pos;
+};
+size_t jobs_table_bytes(int max_jobs, int max_pos);
+JobTable jobs_table(void* base, int max_jobs, int max_pos);
+hipError_t launch_jobs_init(JobTable t, hipStream_t st);
+hipError_t launch_jobs_start(JobTable t, const int32_t* slots, const int64_t* arrival, int m, hipStream_t st);
+hipError_t launch_jobs_append(JobTable t, const int32_t* slots, const int32_t* off, const int32_t* tokens, int m,
+                              int total, hipStream_t st);
+hipError_t launch_jobs_pack(JobTable t, const int32_t* slots, int n, int total, int max_seqlen, int32_t* ids,
+                            int32_t* cu, hipStream_t st);
+hipError_t launch_jobs_store_pred(JobTable t, const int32_t* slots, const float* pred, int n, hipStream_t st);
+size_t jobs_select_workspace_bytes(int max_active);
+hipError_t launch_jobs_select(JobTable t, const int32_t* slots, int a, int k, int32_t* out_slots, int32_t* out_count,
+                              void* workspace, hipStream_t st);
+
 }  // namespace elis

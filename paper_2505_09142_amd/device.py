@@ -128,3 +128,48 @@ def upload_batch(batch, device="cuda"):
     """(token_ids, cu_seqlens, arrival_seq) of a packed batch as device tensors."""
     return (torch.from_numpy(batch.token_ids).to(device), torch.from_numpy(batch.cu_seqlens).to(device),
             torch.from_numpy(batch.arrival_seq).to(device))
+
+
+class JobTable:
+    """Device-resident job table (elis_jobs_*): per job slot the first token, a ring of the most
+    recent max_pos - 1 tokens, the length, the cached prediction and the arrival number."""
+
+    def __init__(self, max_jobs: int, max_pos: int, device="cuda", stream=None):
+        nbytes = E.elis_jobs_table_bytes(max_jobs, max_pos)
+        if nbytes == 0:
+            raise E.ElisError(E.ELIS_EINVAL, "elis_jobs_table_bytes")
+        self.device = device
+        self.buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        base = (self.buf.data_ptr() + 255) // 256 * 256
+        self.t = E.elis_job_table(base, max_jobs, max_pos)
+        self.max_jobs, self.max_pos = max_jobs, max_pos
+        self.sel_ws = Workspace(device)
+        E.check(E.elis_jobs_init(self.t, _stream(stream)), "elis_jobs_init")
+
+    def start(self, slots: torch.Tensor, arrival: torch.Tensor, stream=None):
+        E.check(E.elis_jobs_start(self.t, slots.data_ptr(), arrival.data_ptr(), slots.numel(), _stream(stream)),
+                "elis_jobs_start")
+
+    def append(self, slots: torch.Tensor, offsets: torch.Tensor, tokens: torch.Tensor, total: int, stream=None):
+        E.check(E.elis_jobs_append(self.t, slots.data_ptr(), offsets.data_ptr(),
+                                   tokens.data_ptr() if total > 0 else None, slots.numel(), total, _stream(stream)),
+                "elis_jobs_append")
+
+    def pack(self, slots: torch.Tensor, total: int, max_seqlen: int, out_ids: torch.Tensor, out_cu: torch.Tensor,
+             stream=None):
+        E.check(E.elis_jobs_pack(self.t, slots.data_ptr(), slots.numel(), total, max_seqlen, out_ids.data_ptr(),
+                                 out_cu.data_ptr(), _stream(stream)), "elis_jobs_pack")
+
+    def store_pred(self, slots: torch.Tensor, pred: torch.Tensor, stream=None):
+        E.check(E.elis_jobs_store_pred(self.t, slots.data_ptr(), pred.data_ptr(), slots.numel(), _stream(stream)),
+                "elis_jobs_store_pred")
+
+    def select(self, slots: torch.Tensor, batch_cap: int, out_slots: torch.Tensor, out_count: torch.Tensor,
+               stream=None):
+        a = slots.numel()
+        ws, wsb = self.sel_ws.get(E.elis_jobs_select_workspace_bytes(a))
+        E.check(E.elis_jobs_select(self.t, slots.data_ptr(), a, batch_cap, out_slots.data_ptr(), out_count.data_ptr(),
+                                   ws, wsb, _stream(stream)), "elis_jobs_select")
+
+    def status(self, stream=None):
+        return E.elis_read_status(self.t.base, _stream(stream))

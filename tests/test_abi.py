@@ -171,3 +171,33 @@ def test_timing_api_host_only(lib):
     st, n, ms = E.elis_timing_read(0)
     assert st == 0 and n == 0 and ms == 0.0
     assert E.elis_timing_read(99)[0] == E.ELIS_EINVAL
+
+
+def test_job_table_rejects_invalid_arguments(lib):
+    assert E.elis_jobs_table_bytes(0, 8) == 0
+    assert E.elis_jobs_table_bytes(4, 1) == 0
+    assert E.elis_jobs_table_bytes(100, 512) >= 100 * 511 * 4
+    assert E.elis_jobs_select_workspace_bytes(0) == 0
+    assert E.elis_jobs_select_workspace_bytes(100) >= 100 * (4 + 8 + 4)
+    good = E.elis_job_table(FAKE_WS, 16, 8)
+    assert E.elis_jobs_init(None, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_init(E.elis_job_table(None, 16, 8), None) == E.ELIS_EINVAL
+    assert E.elis_jobs_init(E.elis_job_table(FAKE_WS + 4, 16, 8), None) == E.ELIS_EINVAL   # unaligned
+    assert E.elis_jobs_init(E.elis_job_table(FAKE_WS, 0, 8), None) == E.ELIS_EINVAL
+    assert E.elis_jobs_init(E.elis_job_table(FAKE_WS, 16, 1), None) == E.ELIS_EINVAL
+    assert E.elis_jobs_start(good, None, FAKE, 2, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_start(good, FAKE, FAKE, -1, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_start(good, None, None, 0, None) == E.ELIS_OK                        # nothing to do
+    assert E.elis_jobs_append(good, FAKE, FAKE, None, 2, 3, None) == E.ELIS_EINVAL           # tokens missing
+    assert E.elis_jobs_append(good, FAKE, FAKE, FAKE, 2, -1, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_append(good, None, None, None, 0, 0, None) == E.ELIS_OK
+    assert E.elis_jobs_pack(good, FAKE, 0, 4, 4, FAKE, FAKE, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_pack(good, FAKE, 2, 1, 4, FAKE, FAKE, None) == E.ELIS_ESHAPE          # fewer tokens than jobs
+    assert E.elis_jobs_pack(good, FAKE, 2, 4, 9, FAKE, FAKE, None) == E.ELIS_ESHAPE          # max_seqlen > max_pos
+    assert E.elis_jobs_store_pred(good, FAKE, None, 2, None) == E.ELIS_EINVAL
+    ws = E.elis_jobs_select_workspace_bytes(100)
+    assert E.elis_jobs_select(good, FAKE, 100, 4, FAKE, FAKE, FAKE_WS, ws - 1, None) == E.ELIS_EWORKSPACE
+    assert E.elis_jobs_select(good, FAKE, 0, 4, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_select(good, FAKE, 100, -1, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
+    big = E.elis_jobs_select_workspace_bytes(10000)
+    assert E.elis_jobs_select(good, FAKE, 10000, 9000, FAKE, FAKE, FAKE_WS, big, None) == E.ELIS_EUNSUPPORTED

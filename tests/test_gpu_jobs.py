@@ -1,0 +1,184 @@
+"""Device-resident job table and the scheduling loop built on it.
+
+* Packing: after random appends (prompts longer than the position table
+  included, some appended in one call), the packed token_ids / cu_seqlens of
+  random re-score sets equal the oracle's predictor inputs (first token plus
+  the most recent max_pos - 1 past the table) bit for bit.
+* Selection over cached predictions equals the oracle select on the gathered
+  (prediction, arrival) of the active jobs, up to 10000 active jobs.
+* Content errors (bad slot, host sizes that disagree with the table) set
+  status bits while every kernel still exits normally.
+* The ISRTF loop on the device table reproduces the oracle simulator's
+  trajectory round by round when the oracle is fed the same predictions, and
+  its predictions equal those of the host-packing driver bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.simulate import job_input
+from paper_2505_09142_amd import _elis as E
+from paper_2505_09142_amd.device import JobTable
+from paper_2505_09142_amd.driver import DeviceRoundDriver, HostRoundDriver
+from paper_2505_09142_amd.scheduler import run_isrtf
+from tests.gpu_util import note
+from tests.test_gpu_predict import predictor
+from workloads import S_ISRTF, make_requests
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev(a, dtype):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=dtype)).cuda()
+
+
+def _append(tab, slots, chunks):
+    offs = np.concatenate([[0], np.cumsum([len(c) for c in chunks])]).astype(np.int32)
+    toks = np.concatenate(chunks).astype(np.int32) if offs[-1] else np.zeros(1, np.int32)
+    tab.append(_dev(slots, np.int32), _dev(offs, np.int32), _dev(toks, np.int32), int(offs[-1]))
+
+
+def _pack(tab, slots, lens, max_pos):
+    L = np.minimum(lens, max_pos)
+    T, mx = int(L.sum()), int(L.max())
+    ids = torch.full((T,), -1, dtype=torch.int32, device="cuda")
+    cu = torch.full((len(slots) + 1,), -1, dtype=torch.int32, device="cuda")
+    tab.pack(_dev(slots, np.int32), T, mx, ids, cu)
+    torch.cuda.synchronize()
+    return ids.cpu().numpy(), cu.cpu().numpy()
+
+
+@pytest.mark.parametrize("max_pos", [2, 16, 128])
+def test_pack_matches_oracle_inputs(max_pos):
+    rng = np.random.default_rng(max_pos)
+    J = 64
+    tab = JobTable(J, max_pos)
+    seqs = {}  # slot -> full token list so far
+    slots = rng.permutation(J)[:48]
+    tab.start(_dev(slots, np.int32), _dev(np.arange(48), np.int64))
+    for s in slots:
+        seqs[int(s)] = []
+    for rnd in range(8):
+        # a random subset gains tokens: the first round prompts of up to 3 * max_pos tokens
+        grow = rng.permutation(slots)[:int(rng.integers(1, len(slots)))]
+        chunks = []
+        for s in grow:
+            k = int(rng.integers(1, 3 * max_pos + 2)) if rnd == 0 else int(rng.integers(0, 8))
+            c = rng.integers(1, 30000, size=k).astype(np.int32)
+            seqs[int(s)].extend(c.tolist())
+            chunks.append(c)
+        _append(tab, grow, chunks)
+        live = [int(s) for s in slots if seqs[int(s)]]
+        pick = rng.permutation(live)[:int(rng.integers(1, len(live) + 1))]
+        lens = np.array([len(seqs[int(s)]) for s in pick])
+        note(f"pack max_pos={max_pos} round {rnd}: {len(pick)} jobs, T={int(np.minimum(lens, max_pos).sum())}")
+        ids, cu = _pack(tab, pick, lens, max_pos)
+        exp = [job_input(np.array(seqs[int(s)], np.int32), np.zeros(0, np.int32), 0, max_pos) for s in pick]
+        assert np.array_equal(cu, np.concatenate([[0], np.cumsum([len(x) for x in exp])]))
+        assert np.array_equal(ids, np.concatenate(exp))
+        st, bits = tab.status()
+        assert st == E.ELIS_OK and bits == 0
+
+
+@pytest.mark.parametrize("a", [1, 700, 3000, 10000])
+def test_select_over_table_matches_oracle(a):
+    rng = np.random.default_rng(a)
+    J = max(2 * a, 64)
+    tab = JobTable(J, 8)
+    slots = rng.permutation(J)[:a].astype(np.int32)
+    arrival = rng.integers(0, max(2, a // 3), size=a).astype(np.int64)  # repeated arrivals too
+    pred = rng.integers(0, 50, size=a).astype(np.float32)               # many ties
+    pred[rng.random(a) < 0.01] = np.nan
+    tab.start(_dev(slots, np.int32), _dev(arrival, np.int64))
+    tab.store_pred(_dev(slots, np.int32), _dev(pred, np.float32))
+    for cap in (0, 1, 32, min(a, 8192)):
+        note(f"table select a={a} cap={cap}")
+        out = torch.full((max(1, cap),), -1, dtype=torch.int32, device="cuda")
+        cnt = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        tab.select(_dev(slots, np.int32), cap, out, cnt)
+        torch.cuda.synchronize()
+        m = int(cnt.item())
+        assert m == min(cap, a)
+        exp = slots[oracle.oracle_select(pred, arrival, cap)]
+        assert np.array_equal(out.cpu().numpy()[:m], exp)
+    st, bits = tab.status()
+    assert st == E.ELIS_OK and bits == 0
+
+
+def test_table_content_errors_are_flagged():
+    tab = JobTable(16, 8)
+    tab.start(_dev([0, 1], np.int32), _dev([0, 1], np.int64))
+    _append(tab, np.array([0, 1]), [np.array([5, 6, 7]), np.array([9])])
+    note("job table: slot out of range")
+    tab.store_pred(_dev([3, 99], np.int32), _dev([1.0, 2.0], np.float32))
+    st, bits = tab.status()
+    assert st == E.ELIS_EDEVICE and bits & E.ELIS_DEV_BAD_SLOT
+    E.check(E.elis_jobs_init(tab.t, None))
+    tab.start(_dev([0, 1], np.int32), _dev([0, 1], np.int64))
+    _append(tab, np.array([0, 1]), [np.array([5, 6, 7]), np.array([9])])
+    note("job table: host total disagrees with the table")
+    ids = torch.zeros(8, dtype=torch.int32, device="cuda")
+    cu = torch.zeros(3, dtype=torch.int32, device="cuda")
+    tab.pack(_dev([0, 1], np.int32), 5, 3, ids, cu)  # the table holds 3 + 1 = 4 tokens
+    st, bits = tab.status()
+    assert st == E.ELIS_EDEVICE and bits & E.ELIS_DEV_PACK_SIZE
+    E.check(E.elis_jobs_init(tab.t, None))
+    st, bits = tab.status()
+    assert st == E.ELIS_OK and bits == 0
+
+
+class _Recorder:
+    """Wraps a round driver and keeps what each predict call packed (device path)."""
+
+    def __init__(self, drv):
+        self.drv = drv
+        self.packed = []
+
+    def __getattr__(self, k):
+        return getattr(self.drv, k)
+
+    def predict(self, jobs, out_pred=None):
+        p = self.drv.predict(jobs, out_pred)
+        n = len(jobs)
+        cu = self.drv._cu[:n + 1].cpu().numpy()
+        self.packed.append((self.drv._ids[:int(cu[-1])].cpu().numpy(), cu))
+        return p
+
+
+def test_device_scheduler_matches_oracle_trajectory():
+    s = S_ISRTF
+    W, pr = predictor(s.shape, s.weight_seed)
+    req = make_requests(s)
+    rounds = 160
+    dev = _Recorder(DeviceRoundDriver(pr, 1024, s.shape.max_pos))
+    got = run_isrtf(req.arrival_t, req.prompt, req.response, dev, window=s.window, step_cost=s.step_cost_s,
+                    batch_cap=s.batch_cap, max_rounds=rounds)
+    host = run_isrtf(req.arrival_t, req.prompt, req.response, HostRoundDriver(pr, s.shape.max_pos, len(req.prompt)),
+                     window=s.window, step_cost=s.step_cost_s, batch_cap=s.batch_cap, max_rounds=rounds)
+    replay = iter([r.pred for r in got.rounds if len(r.rescored)])
+    packed = iter(dev.packed)
+    checked = {"inputs": 0}
+
+    def predict_fn(todo, inputs, g):
+        ids, cu = next(packed)
+        assert np.array_equal(cu, np.concatenate([[0], np.cumsum([len(x) for x in inputs])]))
+        assert np.array_equal(ids, np.concatenate(inputs))
+        checked["inputs"] += 1
+        return next(replay)
+
+    ref = oracle.simulate(req.arrival_t, req.prompt, req.response, window=s.window, step_cost=s.step_cost_s,
+                          batch_cap=s.batch_cap, max_pos=s.shape.max_pos, predict_fn=predict_fn,
+                          max_rounds=rounds)
+    assert len(got.rounds) == len(ref.rounds) == len(host.rounds) == rounds
+    for i, (a, b, h) in enumerate(zip(got.rounds, ref.rounds, host.rounds)):
+        assert a.t == b.t and list(a.rescored) == list(b.rescored), i
+        assert list(a.candidates) == list(b.candidates) and list(a.chosen) == list(b.selected), i
+        assert a.steps == b.window_steps, i
+        assert list(h.chosen) == list(a.chosen) and np.array_equal(h.pred.view(np.uint32), a.pred.view(np.uint32)), i
+    assert np.array_equal(got.generated, ref.generated)
+    note(f"device loop: {rounds} rounds, {checked['inputs']} packed re-score sets equal the oracle inputs, "
+         f"p50 round {1e3 * np.median([r.latency_s for r in got.rounds]):.2f} ms "
+         f"(host packing {1e3 * np.median([r.latency_s for r in host.rounds]):.2f} ms)")
+    st, bits = dev.drv.table.status()
+    assert st == E.ELIS_OK and bits == 0
