@@ -29,6 +29,28 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
+def _head_params(s):
+    nl, hh, d = s.n_head_layers, s.head_hidden, s.d_model
+    if nl == 1:
+        return d + 1
+    return hh * d + hh + (nl - 2) * (hh * hh + hh) + hh + 1
+
+
+def _describe(w):
+    s = w.shape
+    pool = "CLS" if s.pooling == 0 else "mean"
+    if s.n_head_layers == 1:
+        head = f"{s.d_model}->1"
+    elif s.n_head_layers == 2:
+        head = f"{s.d_model}->{s.head_hidden}->{'ReLU' if s.head_act == 0 else 'linear'}->1"
+    else:
+        head = (f"{s.n_head_layers} FC layers, width {s.head_hidden}, "
+                f"{'ReLU' if s.head_act == 0 else 'no activation'}")
+    return (f"{w.name}: {s.name}-shaped predictor ({s.n_layers} layers, d_model {s.d_model}, {s.n_heads} heads, "
+            f"FFN {s.d_ff}, {pool} pooling, head {head}), {w.n_seqs} packed in-flight sequences, ISRTF select "
+            f"{w.batch_cap} of {w.n_seqs}")
+
+
 def _algorithmic(w, b):
     """Per-launch algorithmic FLOPs (contractions) or bytes (row kernels) by kernel class."""
     s = w.shape
@@ -45,7 +67,8 @@ def _algorithmic(w, b):
         "layernorm": ("byte", T * (d * (4.0 + 2.0) + 8.0), 2 * L),
         # ids + gathered bf16 word and position rows in; fp32 pre-norm + bf16 rows + stats out
         "embed_ln": ("byte", T * (4.0 + d * (2.0 + 2.0 + 4.0 + 2.0) + 8.0), 1),
-        "pool_head": ("byte", n * d * 4.0 + (s.head_hidden or 1) * d * 4.0, 1),
+        # pooled rows in + every head weight once
+        "pool_head": ("byte", n * d * 4.0 + 4.0 * _head_params(s), 1),
         "seqmap": ("byte", (n + 1) * 4.0 * 4, 1),
         "select": ("byte", n * 12.0 + w.batch_cap * 4.0, 1),
     }
@@ -541,9 +564,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: BERT-base-shaped predictor (12 layers, d_model 768, 12 heads, FFN 3072, "
-                               f"CLS pooling, 768->256->1 head), {n} packed in-flight sequences, ISRTF select "
-                               f"{w.batch_cap} of {n}",
+        "config": {"workload": _describe(w),
                    "n_seqs": n, "total_tokens": T, "max_seqlen": msl, "batch_cap": w.batch_cap,
                    "global_batch": n, "seq_len": msl, "parallelism": "none (1 GPU)"},
         "tokens_per_s": T * args.steps / elapsed,

@@ -56,16 +56,29 @@ extern "C" {
 #define ELIS_POOL_CLS  0 /* the first token's final hidden vector (Sec. 3.2)              */
 #define ELIS_POOL_MEAN 1 /* the mean of all of a sequence's final hidden vectors (Sec. 4.2) */
 
+#define ELIS_ACT_RELU     0 /* ReLU between the head's FC layers (Sec. 4.2)           */
+#define ELIS_ACT_IDENTITY 1 /* no activation: a stack of linear layers (Sec. 3.2)     */
+
 /*
  * Encoder shape. Supported by this build: d_model % 64 == 0, d_model <= 2048,
- * d_ff % 64 == 0, d_model / n_heads in {32, 64}, n_layers >= 0, head_hidden
- * in [0, 4096]. Anything else returns ELIS_EUNSUPPORTED (or ELIS_EINVAL for
- * non-positive sizes).
+ * d_ff % 64 == 0, d_model / n_heads in {32, 64}, n_layers >= 0; head_layers
+ * in [1, 16] with head_hidden == 0 when head_layers == 1 and head_hidden a
+ * multiple of 4 in [4, 4096] otherwise. Anything else returns
+ * ELIS_EUNSUPPORTED (or ELIS_EINVAL for non-positive sizes).
+ *
+ * The regression head is head_layers fully connected layers on the pooled
+ * vector z: one layer d->1; or d->head_hidden, then head_layers - 2 layers
+ * head_hidden->head_hidden, then head_hidden->1, with head_act between
+ * consecutive layers (the paper's heads: d->256->ReLU->1 style; eight FC layers
+ * of width 1024 with ReLU on mean pooling, Sec. 4.2; eight linear layers on
+ * the CLS vector, Sec. 3.2).
  */
 typedef struct elis_config {
     int32_t n_layers, d_model, n_heads, d_ff, vocab, max_pos;
     int32_t pooling;      /* ELIS_POOL_CLS or ELIS_POOL_MEAN                        */
-    int32_t head_hidden;  /* 0: linear d->1; else d->head_hidden->ReLU->1           */
+    int32_t head_hidden;  /* width of the head's hidden layers (0: one layer d->1)  */
+    int32_t head_layers;  /* fully connected layers of the head (>= 1)              */
+    int32_t head_act;     /* ELIS_ACT_RELU or ELIS_ACT_IDENTITY                     */
     float ln_eps;         /* LayerNorm epsilon (biased variance)                   */
     float out_scale, out_shift; /* prediction = out_shift + out_scale * head output */
 } elis_config;
@@ -88,10 +101,14 @@ typedef struct elis_weights {
     const float *type0;    /* fp32 [d]          token-type-0 row, added to all  */
     const float *emb_ln_g, *emb_ln_b;          /* fp32 [d] embedding LayerNorm  */
     const elis_layer_weights *layers;          /* HOST array of n_layers entries */
-    const float *head_w1;  /* fp32 [head_hidden, d] (unused when head_hidden == 0) */
-    const float *head_b1;  /* fp32 [head_hidden]                                   */
-    const float *head_w2;  /* fp32 [1, head_hidden] or [1, d] for the linear head  */
-    const float *head_b2;  /* fp32 [1]                                             */
+    const float *head_w1;  /* fp32 [head_hidden, d]: first layer (head_layers >= 2)   */
+    const float *head_b1;  /* fp32 [head_hidden]                                      */
+    const float *head_w2;  /* fp32 [1, head_hidden], or [1, d] when head_layers == 1  */
+    const float *head_b2;  /* fp32 [1]                                                */
+    const float *const *head_mid_w; /* HOST array of head_layers - 2 device pointers,
+                                       fp32 [head_hidden, head_hidden] each (NULL if none) */
+    const float *const *head_mid_b; /* HOST array of head_layers - 2 device pointers,
+                                       fp32 [head_hidden] each                           */
 } elis_weights;
 
 /*
@@ -304,7 +321,7 @@ int elis_timing_enable(uint32_t class_mask); /* bit c enables class c; 0 disable
 int elis_timing_reset(void);
 int elis_timing_read(int32_t kernel_class, int32_t *launches, double *total_ms);
 
-/* ABI version of this header: 1. */
+/* ABI version of this header: 2. */
 int32_t elis_abi_version(void);
 
 #ifdef __cplusplus

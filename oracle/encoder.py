@@ -105,13 +105,28 @@ def pool(h: np.ndarray, pooling: int) -> np.ndarray:
     raise ValueError(pooling)
 
 
+def _head_layers(shape) -> int:
+    n = getattr(shape, "head_layers", 0)
+    if n:
+        return n
+    return 2 if shape.head_hidden else 1
+
+
 def regression_head(z: np.ndarray, m: dict, shape) -> float:
-    """Linear head, or one hidden ReLU layer, to a scalar; then the affine map to tokens."""
-    if shape.head_hidden:
-        hid = np.maximum(_f64(m["head_w1"]) @ z + _f64(m["head_b1"]), 0.0)
-    else:
-        hid = z
-    y = float(_f64(m["head_w2"])[0] @ hid + _f64(m["head_b2"])[0])
+    """Fully connected layers on the pooled vector, then the affine map to tokens.
+
+    One layer: y = w2 . z + b2. More: h = act(W1 z + b1), then head_layers - 2 times
+    h = act(Wl h + bl), then y = w2 . h + b2, with act = ReLU (Sec. 4.2) or none
+    (a stack of linear layers, Sec. 3.2)."""
+    nl = _head_layers(shape)
+    relu = getattr(shape, "head_act", 0) == 0
+    act = (lambda v: np.maximum(v, 0.0)) if relu else (lambda v: v)
+    h = z
+    if nl >= 2:
+        h = act(_f64(m["head_w1"]) @ h + _f64(m["head_b1"]))
+        for w, b in zip(m.get("head_mid_w", []), m.get("head_mid_b", [])):
+            h = act(_f64(w) @ h + _f64(b))
+    y = float(_f64(m["head_w2"])[0] @ h + _f64(m["head_b2"])[0])
     return shape.out_shift + shape.out_scale * y
 
 

@@ -31,6 +31,8 @@ ELIS_DEV_PACK_SIZE = 16
 ELIS_POOL_CLS = 0
 ELIS_POOL_MEAN = 1
 
+ELIS_ACT_RELU = 0
+ELIS_ACT_IDENTITY = 1
 ELIS_EPI_BIAS_BF16 = 0
 ELIS_EPI_BIAS_GELU_BF16 = 1
 ELIS_EPI_BIAS_RES_F32 = 2
@@ -53,6 +55,7 @@ class ElisError(RuntimeError):
 class elis_config(ctypes.Structure):
     _fields_ = [("n_layers", c_int32), ("d_model", c_int32), ("n_heads", c_int32), ("d_ff", c_int32),
                 ("vocab", c_int32), ("max_pos", c_int32), ("pooling", c_int32), ("head_hidden", c_int32),
+                ("head_layers", c_int32), ("head_act", c_int32),
                 ("ln_eps", c_float), ("out_scale", c_float), ("out_shift", c_float)]
 
 
@@ -64,7 +67,8 @@ class elis_layer_weights(ctypes.Structure):
 class elis_weights(ctypes.Structure):
     _fields_ = [("cfg", elis_config), ("word", c_void_p), ("pos", c_void_p), ("type0", c_void_p),
                 ("emb_ln_g", c_void_p), ("emb_ln_b", c_void_p), ("layers", POINTER(elis_layer_weights)),
-                ("head_w1", c_void_p), ("head_b1", c_void_p), ("head_w2", c_void_p), ("head_b2", c_void_p)]
+                ("head_w1", c_void_p), ("head_b1", c_void_p), ("head_w2", c_void_p), ("head_b2", c_void_p),
+                ("head_mid_w", POINTER(c_void_p)), ("head_mid_b", POINTER(c_void_p))]
 
 
 class elis_job_table(ctypes.Structure):

@@ -59,14 +59,16 @@ int status_of(hipError_t e) {
 int check_config(const elis_config* c) {
     if (!c) return ELIS_EINVAL;
     if (c->n_layers < 0 || c->d_model <= 0 || c->n_heads <= 0 || c->d_ff <= 0 || c->vocab <= 0 ||
-        c->max_pos <= 0 || c->head_hidden < 0)
+        c->max_pos <= 0 || c->head_hidden < 0 || c->head_layers < 1)
         return ELIS_EINVAL;
+    if (c->head_act != ELIS_ACT_RELU && c->head_act != ELIS_ACT_IDENTITY) return ELIS_EINVAL;
+    if ((c->head_layers == 1) != (c->head_hidden == 0)) return ELIS_EINVAL;
     if (c->pooling != ELIS_POOL_CLS && c->pooling != ELIS_POOL_MEAN) return ELIS_EINVAL;
     if (!(c->ln_eps >= 0.f) || !isfinite(c->out_scale) || !isfinite(c->out_shift)) return ELIS_EINVAL;
     if (c->d_model % 64 || c->d_model > 2048 || c->d_ff % 64 || c->d_model % c->n_heads) return ELIS_EUNSUPPORTED;
     const int dh = c->d_model / c->n_heads;
     if (dh != 32 && dh != 64) return ELIS_EUNSUPPORTED;
-    if (c->head_hidden > 4096) return ELIS_EUNSUPPORTED;
+    if (c->head_hidden > 4096 || c->head_hidden % 4 || c->head_layers > 16) return ELIS_EUNSUPPORTED;
     return ELIS_OK;
 }
 
@@ -76,7 +78,12 @@ int check_weights(const elis_weights* w) {
     if (r != ELIS_OK) return r;
     if (!w->word || !w->pos || !w->type0 || !w->emb_ln_g || !w->emb_ln_b || !w->head_w2 || !w->head_b2)
         return ELIS_EINVAL;
-    if (w->cfg.head_hidden > 0 && (!w->head_w1 || !w->head_b1)) return ELIS_EINVAL;
+    if (w->cfg.head_layers >= 2 && (!w->head_w1 || !w->head_b1)) return ELIS_EINVAL;
+    if (w->cfg.head_layers > 2) {
+        if (!w->head_mid_w || !w->head_mid_b) return ELIS_EINVAL;
+        for (int l = 0; l < w->cfg.head_layers - 2; ++l)
+            if (!w->head_mid_w[l] || !w->head_mid_b[l]) return ELIS_EINVAL;
+    }
     if (w->cfg.n_layers > 0 && !w->layers) return ELIS_EINVAL;
     for (int l = 0; l < w->cfg.n_layers; ++l) {
         const elis_layer_weights& y = w->layers[l];
@@ -125,7 +132,8 @@ PredictLayout predict_layout(const elis_config& c, int T, int n, int max_seqlen)
         p.pool_partial = take(sizeof(float) * static_cast<size_t>(n) * p.nchunk * d);
         p.pool_z = take(sizeof(float) * static_cast<size_t>(n) * d);
     }
-    if (c.head_hidden > 0) p.head_hid = take(sizeof(float) * static_cast<size_t>(n) * c.head_hidden);
+    if (c.head_layers >= 2)
+        p.head_hid = take(sizeof(float) * static_cast<size_t>(n) * c.head_hidden * (c.head_layers > 2 ? 2 : 1));
     p.total = o;
     return p;
 }
@@ -143,7 +151,7 @@ T* at(void* base, size_t off) {
 
 extern "C" {
 
-int32_t elis_abi_version(void) { return 1; }
+int32_t elis_abi_version(void) { return 2; }
 
 const char* elis_status_string(int s) {
     switch (s) {
@@ -245,11 +253,13 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
         prev_b = y.ln2_b;
     }
     e = timed(ELIS_K_POOL_HEAD, st, [&] {
+        float* hid = c.head_layers >= 2 ? at<float>(workspace, p.head_hid) : nullptr;
         const PoolScratch scr{c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_partial) : nullptr,
-                              c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_z) : nullptr,
-                              c.head_hidden > 0 ? at<float>(workspace, p.head_hid) : nullptr, p.nchunk};
-        return launch_pool_head(final32, tab, n, d, c.pooling, c.head_hidden, w->head_w1, w->head_b1, w->head_w2,
-                                w->head_b2, c.out_scale, c.out_shift, out_pred, scr, st);
+                              c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_z) : nullptr, hid,
+                              c.head_layers > 2 ? hid + static_cast<size_t>(n) * c.head_hidden : nullptr, p.nchunk};
+        const HeadSpec head{c.head_layers, c.head_hidden, c.head_act, w->head_w1, w->head_b1, w->head_w2,
+                            w->head_b2, w->head_mid_w, w->head_mid_b};
+        return launch_pool_head(final32, tab, n, d, c.pooling, head, c.out_scale, c.out_shift, out_pred, scr, st);
     });
     return status_of(e);
 }

@@ -59,11 +59,18 @@ constexpr int kPoolChunk = 64;  // rows per partial sum of mean pooling
 struct PoolScratch {
     float* partial;  // [n, nchunk, d]   (mean pooling)
     float* z;        // [n, d]           (mean pooling)
-    float* hid;      // [n, head_hidden] (MLP head)
+    float* hid;      // [n, head_hidden] (multi-layer head)
+    float* hid2;     // [n, head_hidden] (more than two layers: the other ping-pong buffer)
     int nchunk;      // ceil(max_seqlen / kPoolChunk)
 };
-hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int pooling, int head_hidden,
-                            const float* w1, const float* b1, const float* w2, const float* b2,
+// The regression head: `layers` FC layers, hidden width `hidden`, activation `act`.
+struct HeadSpec {
+    int layers, hidden, act;
+    const float *w1, *b1, *w2, *b2;
+    const float* const* mid_w;  // host array of layers - 2 device pointers
+    const float* const* mid_b;
+};
+hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int pooling, const HeadSpec& head,
                             float scale, float shift, float* out, PoolScratch scr, hipStream_t st);
 
 // select.hip

@@ -2,16 +2,19 @@
 //
 // CLS pooling takes the sequence's first final hidden vector (Sec. 3.2); mean
 // pooling averages all of them, the CLS position included (Sec. 4.2). The head
-// is linear d->1 or d->hidden->ReLU->1 in fp32; the result is mapped to tokens
-// as shift + scale * y.
+// is a stack of fully connected fp32 layers: d->1, or d->hidden, hidden->hidden
+// (head_layers - 2 times), hidden->1, with ReLU or no activation between layers
+// (the paper's eight-layer, width-1024 head, Sec. 4.2); the result is mapped
+// to tokens as shift + scale * y.
 //
 // Kernels (all reductions in a fixed order, so results are bitwise
 // reproducible and independent of how sequences are packed):
 //   pool_partial  mean pooling only: per (sequence, 256-column block, 64-row
 //                 chunk) column sums, fully coalesced row reads;
 //   pool_reduce   mean pooling only: chunk sums in order, divided by the length;
-//   head_hidden   MLP head only: one wave per (hidden unit, 4 sequences), lanes
-//                 across d, so each weight row is read once per 4 sequences;
+//   head_fc       every layer of a multi-layer head but the last: one wave per
+//                 (output unit, 8 sequences), lanes across the inputs,
+//                 ping-ponging between two [n, hidden] buffers;
 //   head_out      one wave per sequence: ReLU(hidden + b1) . w2 + b2 (or z . w
 //                 + b for the linear head), then shift + scale * y.
 // For CLS pooling the head reads the CLS row of the hidden states in place.
@@ -22,7 +25,13 @@ namespace elis {
 namespace {
 
 constexpr int kCols = 256;      // columns per pooling work-group
-constexpr int kSeqPerWave = 4;  // sequences sharing one weight-row read in head_hidden
+constexpr int kFcSeq = 8;  // sequences sharing one weight-row read in head_fc
+
+template <int ACT>
+__device__ __forceinline__ float act(float x) {
+    if constexpr (ACT == ELIS_ACT_RELU) return fmaxf(x, 0.f);
+    return x;
+}
 
 __global__ __launch_bounds__(kCols) void pool_partial_kernel(const float* __restrict__ hidden,
                                                              const int32_t* __restrict__ start,
@@ -68,32 +77,41 @@ __device__ __forceinline__ const float* pooled_row(int s, int pooling, const flo
     return pooling == ELIS_POOL_CLS ? hidden + static_cast<size_t>(start[s]) * d : z + static_cast<size_t>(s) * d;
 }
 
-// grid (hh, ceil(n / kSeqPerWave)), one wave per work-group.
-__global__ __launch_bounds__(kWave) void head_hidden_kernel(const float* __restrict__ hidden,
-                                                            const float* __restrict__ z,
-                                                            const int32_t* __restrict__ start, int n, int d,
-                                                            int pooling, int hh, const float* __restrict__ w1,
-                                                            const float* __restrict__ b1,
-                                                            float* __restrict__ hid) {
-    const int j = blockIdx.x, s0 = blockIdx.y * kSeqPerWave, lane = threadIdx.x;
-    const float* wr = w1 + static_cast<size_t>(j) * d;
-    const float* zr[kSeqPerWave];
+// One fully connected layer of the head, out[s, j] = act(x[s, :] . w[j, :] + b[j]), K inputs,
+// N outputs: one wave per (output unit, kFcSeq sequences), lanes across K, so a weight row is
+// read once per kFcSeq sequences. Many small waves (N * n / kFcSeq) keep load latency hidden;
+// the input rows (the pooled rows for the first layer, else the previous layer's output) are
+// re-read per unit from L2, which measured cheaper than staging them in LDS for fewer waves.
+// grid (N, ceil(n / kFcSeq)), one wave per work-group.
+template <int ACT, bool POOLED>
+__global__ __launch_bounds__(kWave) void head_fc_kernel(const float* __restrict__ in, const float* __restrict__ hidden,
+                                                        const float* __restrict__ z, const int32_t* __restrict__ start,
+                                                        int pooling, int n, int K, int N,
+                                                        const float* __restrict__ w, const float* __restrict__ b,
+                                                        float* __restrict__ out) {
+    const int j = blockIdx.x, s0 = blockIdx.y * kFcSeq, lane = threadIdx.x;
+    const float* wr = w + static_cast<size_t>(j) * K;
+    const float* xr[kFcSeq];
 #pragma unroll
-    for (int q = 0; q < kSeqPerWave; ++q)
-        zr[q] = pooled_row(s0 + q < n ? s0 + q : n - 1, pooling, hidden, z, start, d);
-    float acc[kSeqPerWave] = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 4 * lane; c < d; c += 4 * kWave) {
-        const f32x4 w = *reinterpret_cast<const f32x4*>(wr + c);
+    for (int q = 0; q < kFcSeq; ++q) {
+        const int s = s0 + q < n ? s0 + q : n - 1;
+        xr[q] = POOLED ? pooled_row(s, pooling, hidden, z, start, K) : in + static_cast<size_t>(s) * K;
+    }
+    float acc[kFcSeq];
 #pragma unroll
-        for (int q = 0; q < kSeqPerWave; ++q) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(zr[q] + c);
-            acc[q] += (w[0] * v[0] + w[1] * v[1]) + (w[2] * v[2] + w[3] * v[3]);
+    for (int q = 0; q < kFcSeq; ++q) acc[q] = 0.f;
+    for (int c = 4 * lane; c < K; c += 4 * kWave) {
+        const f32x4 wv = *reinterpret_cast<const f32x4*>(wr + c);
+#pragma unroll
+        for (int q = 0; q < kFcSeq; ++q) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(xr[q] + c);
+            acc[q] += (wv[0] * v[0] + wv[1] * v[1]) + (wv[2] * v[2] + wv[3] * v[3]);
         }
     }
 #pragma unroll
-    for (int q = 0; q < kSeqPerWave; ++q) {
+    for (int q = 0; q < kFcSeq; ++q) {
         const float t = wave_sum(acc[q]);
-        if (lane == 0 && s0 + q < n) hid[static_cast<size_t>(s0 + q) * hh + j] = fmaxf(t + b1[j], 0.f);
+        if (lane == 0 && s0 + q < n) out[static_cast<size_t>(s0 + q) * N + j] = act<ACT>(t + b[j]);
     }
 }
 
@@ -115,9 +133,30 @@ __global__ __launch_bounds__(kWave) void head_out_kernel(const float* __restrict
 
 }  // namespace
 
-hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int pooling, int head_hidden,
-                            const float* w1, const float* b1, const float* w2, const float* b2, float scale,
-                            float shift, float* out, PoolScratch scr, hipStream_t st) {
+namespace {
+
+template <int ACT, bool POOLED>
+hipError_t fc(const float* in, const float* hidden, const float* z, const int32_t* start, int pooling, int n, int K,
+              int N, const float* w, const float* b, float* out, hipStream_t st) {
+    hipLaunchKernelGGL((head_fc_kernel<ACT, POOLED>), dim3(N, (n + kFcSeq - 1) / kFcSeq), dim3(kWave), 0, st, in,
+                       hidden, z, start, pooling, n, K, N, w, b, out);
+    return hipSuccess;
+}
+
+hipError_t launch_fc(int act, bool pooled, const float* in, const float* hidden, const float* z,
+                     const int32_t* start, int pooling, int n, int K, int N, const float* w, const float* b,
+                     float* out, hipStream_t st) {
+    if (act == ELIS_ACT_RELU)
+        return pooled ? fc<ELIS_ACT_RELU, true>(in, hidden, z, start, pooling, n, K, N, w, b, out, st)
+                      : fc<ELIS_ACT_RELU, false>(in, hidden, z, start, pooling, n, K, N, w, b, out, st);
+    return pooled ? fc<ELIS_ACT_IDENTITY, true>(in, hidden, z, start, pooling, n, K, N, w, b, out, st)
+                  : fc<ELIS_ACT_IDENTITY, false>(in, hidden, z, start, pooling, n, K, N, w, b, out, st);
+}
+
+}  // namespace
+
+hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int pooling, const HeadSpec& head,
+                            float scale, float shift, float* out, PoolScratch scr, hipStream_t st) {
     if (d % 4 != 0) return hipErrorInvalidValue;
     const dim3 cols(n, (d + kCols - 1) / kCols);
     if (pooling == ELIS_POOL_MEAN) {
@@ -125,11 +164,24 @@ hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int
                            tab.len, d, scr.nchunk, scr.partial);
         hipLaunchKernelGGL(pool_reduce_kernel, cols, dim3(kCols), 0, st, scr.partial, tab.len, d, scr.nchunk, scr.z);
     }
-    if (head_hidden > 0)
-        hipLaunchKernelGGL(head_hidden_kernel, dim3(head_hidden, (n + kSeqPerWave - 1) / kSeqPerWave), dim3(kWave), 0,
-                           st, hidden, scr.z, tab.start, n, d, pooling, head_hidden, w1, b1, scr.hid);
-    hipLaunchKernelGGL(head_out_kernel, dim3(n), dim3(kWave), 0, st, hidden, scr.z, tab.start, d, pooling, head_hidden,
-                       scr.hid, w2, b2, scale, shift, out);
+    const int hh = head.layers >= 2 ? head.hidden : 0;
+    float* cur = scr.hid;
+    if (hh > 0) {
+        hipError_t e = launch_fc(head.act, true, nullptr, hidden, scr.z, tab.start, pooling, n, d, hh, head.w1,
+                                 head.b1, cur, st);
+        if (e != hipSuccess) return e;
+        float* nxt = scr.hid2;
+        for (int l = 0; l < head.layers - 2; ++l) {
+            e = launch_fc(head.act, false, cur, nullptr, nullptr, nullptr, pooling, n, hh, hh, head.mid_w[l],
+                          head.mid_b[l], nxt, st);
+            if (e != hipSuccess) return e;
+            float* t = cur;
+            cur = nxt;
+            nxt = t;
+        }
+    }
+    hipLaunchKernelGGL(head_out_kernel, dim3(n), dim3(kWave), 0, st, hidden, scr.z, tab.start, d, pooling, hh, cur,
+                       head.w2, head.b2, scale, shift, out);
     return hipGetLastError();
 }
 

@@ -34,7 +34,8 @@ def _to_dev(a: np.ndarray, device) -> torch.Tensor:
 def config_of(shape) -> E.elis_config:
     """elis_config from any object with the encoder-shape attributes."""
     return E.elis_config(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ff, shape.vocab, shape.max_pos,
-                         shape.pooling, shape.head_hidden, shape.ln_eps, shape.out_scale, shape.out_shift)
+                         shape.pooling, shape.head_hidden, shape.n_head_layers, shape.head_act, shape.ln_eps,
+                         shape.out_scale, shape.out_shift)
 
 
 class DeviceWeights:
@@ -59,9 +60,14 @@ class DeviceWeights:
                          "ln2_b"):
                 setattr(y, name, self.t[name][l].data_ptr())
         p = lambda k: self.t[k].data_ptr() if k in self.t else None
+        nmid = len(self.t.get("head_mid_w", []))
+        self._mid_w = (ctypes.c_void_p * max(1, nmid))(*[x.data_ptr() for x in self.t.get("head_mid_w", [])])
+        self._mid_b = (ctypes.c_void_p * max(1, nmid))(*[x.data_ptr() for x in self.t.get("head_mid_b", [])])
+        mid = lambda a: ctypes.cast(a, ctypes.POINTER(ctypes.c_void_p)) if nmid else None
         self.struct = E.elis_weights(self.cfg, p("word"), p("pos"), p("type0"), p("emb_ln_g"), p("emb_ln_b"),
                                      ctypes.cast(self._layers, ctypes.POINTER(E.elis_layer_weights)),
-                                     p("head_w1"), p("head_b1"), p("head_w2"), p("head_b2"))
+                                     p("head_w1"), p("head_b1"), p("head_w2"), p("head_b2"),
+                                     mid(self._mid_w), mid(self._mid_b))
 
 
 class Workspace:

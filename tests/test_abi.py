@@ -8,7 +8,8 @@ import re
 import pytest
 
 from paper_2505_09142_amd import _elis as E
-from workloads import BERT_BASE, TINY, XLMR_LARGE
+from paper_2505_09142_amd.device import config_of
+from workloads import BERT_BASE, TINY, TINY_HEAD8, XLMR_LARGE
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "elis.h")
@@ -39,16 +40,15 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert E.elis_abi_version() == 1
+    assert E.elis_abi_version() == 2
     for s in (0, -1, -2, -3, -4, -5, -6):
         assert E.elis_status_string(s).startswith("ELIS_")
     assert E.elis_status_string(123) == "unknown status"
 
 
 def test_workspace_queries(lib):
-    for shape in (TINY, BERT_BASE, XLMR_LARGE):
-        cfg = E.elis_config(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ff, shape.vocab, shape.max_pos,
-                            shape.pooling, shape.head_hidden, shape.ln_eps, shape.out_scale, shape.out_shift)
+    for shape in (TINY, BERT_BASE, XLMR_LARGE, TINY_HEAD8):
+        cfg = config_of(shape)
         b = E.elis_predict_workspace_bytes(cfg, 1000, 8, 64)
         d, F = shape.d_model, shape.d_ff
         # fp32 residual + bf16 copy + qkv + attention out + fp32 pre-LN + FFN activation
@@ -72,15 +72,17 @@ def test_workspace_queries(lib):
 
 
 def _weights(shape=TINY):
-    cfg = E.elis_config(shape.n_layers, shape.d_model, shape.n_heads, shape.d_ff, shape.vocab, shape.max_pos,
-                        shape.pooling, shape.head_hidden, shape.ln_eps, shape.out_scale, shape.out_shift)
+    cfg = config_of(shape)
     layers = (E.elis_layer_weights * max(1, shape.n_layers))()
     for l in range(shape.n_layers):
         for f, _ in E.elis_layer_weights._fields_:
             setattr(layers[l], f, FAKE)
+    nmid = max(0, shape.n_head_layers - 2)
+    mid = (ctypes.c_void_p * max(1, nmid))(*([FAKE] * nmid))
+    midp = ctypes.cast(mid, ctypes.POINTER(ctypes.c_void_p)) if nmid else None
     w = E.elis_weights(cfg, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.cast(layers, ctypes.POINTER(E.elis_layer_weights)),
-                       FAKE, FAKE, FAKE, FAKE)
-    w._keep = layers
+                       FAKE, FAKE, FAKE, FAKE, midp, midp)
+    w._keep = (layers, mid)
     return w
 
 
@@ -122,9 +124,24 @@ def test_predict_rejects_bad_config(lib):
     w.layers[1].w_2 = None
     assert _predict(w) == E.ELIS_EINVAL
     w = _weights()
-    w.cfg.head_hidden = 16
-    w.head_w1 = None
+    w.cfg.head_hidden = 16                                       # hidden width with a one-layer head
     assert _predict(w) == E.ELIS_EINVAL
+    w = _weights()
+    w.cfg.head_hidden, w.cfg.head_layers = 16, 2
+    w.head_w1 = None                                             # first layer missing
+    assert _predict(w) == E.ELIS_EINVAL
+    w = _weights(TINY_HEAD8)
+    w.head_mid_w = None                                          # middle layers missing
+    assert _predict(w) == E.ELIS_EINVAL
+    w = _weights(TINY_HEAD8)
+    w.cfg.head_act = 5
+    assert _predict(w) == E.ELIS_EINVAL
+    w = _weights(TINY_HEAD8)
+    w.cfg.head_layers = 0
+    assert _predict(w) == E.ELIS_EINVAL
+    w = _weights(TINY_HEAD8)
+    w.cfg.head_hidden = 66                                       # not a multiple of 4
+    assert _predict(w) == E.ELIS_EUNSUPPORTED
 
 
 def test_select_rejects_invalid_arguments(lib):

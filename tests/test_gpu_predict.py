@@ -17,7 +17,8 @@ import oracle
 from paper_2505_09142_amd import _elis as E
 from paper_2505_09142_amd.device import DeviceWeights, Predictor, upload_batch
 from tests.gpu_util import dev, note
-from workloads import (TINY, W_BERT_B64, W_TINY, W_XLMR_B128, bf16_bits_to_f32, make_batch, make_weights, pack)
+from workloads import (TINY, W_BERT_B64, W_BERT_B64_HEAD8, W_TINY, W_TINY_CLS_LIN8, W_TINY_HEAD8, W_XLMR_B128,
+                       bf16_bits_to_f32, make_batch, make_weights, pack)
 
 pytestmark = pytest.mark.gpu
 
@@ -92,6 +93,23 @@ def test_tiny_end_to_end():
                     np.abs(pred - ref_p).max())
 
 
+@pytest.mark.parametrize("w,n", [(W_TINY_HEAD8, 8), (W_TINY_CLS_LIN8, 8), (W_TINY_HEAD8, 37)])
+def test_tiny_deep_heads_end_to_end(w, n):
+    """The paper's eight-layer heads (mean pooling + ReLU FC, Sec. 4.2; CLS + linear layers,
+    Sec. 3.2) on every sequence; 37 sequences leave ragged groups in the head kernels."""
+    w = dataclasses.replace(w, n_seqs=n, batch_cap=min(w.batch_cap, n))
+    note(f"{w.name} with {n} sequences: eight-layer head, all sequences")
+    W, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    pred, hid, d_arr = run(pr, b)
+    ref_p, ref_h = oracle.oracle_forward(b.token_ids, b.cu_seqlens, W.master, w.shape)
+    herr = np.abs(hid - ref_h).max()
+    perr = rel_err(pred, ref_p).max()
+    note(f"{w.name}: hidden max-abs {herr:.3e}, pred max-rel {perr:.3e}, pred spread {np.ptp(ref_p):.2f}")
+    assert herr <= HIDDEN_ATOL and perr <= PRED_RTOL
+    check_selection(pr, pred, d_arr, b.arrival_seq, w.batch_cap, ref_p, np.abs(pred - ref_p).max())
+
+
 def _sample(lengths, count, seed):
     rng = np.random.default_rng(seed)
     pick = {int(np.argmin(lengths)), int(np.argmax(lengths))}
@@ -100,7 +118,7 @@ def _sample(lengths, count, seed):
     return sorted(pick)
 
 
-@pytest.mark.parametrize("w,count", [(W_BERT_B64, 5), (W_XLMR_B128, 3)])
+@pytest.mark.parametrize("w,count", [(W_BERT_B64, 5), (W_XLMR_B128, 3), (W_BERT_B64_HEAD8, 3)])
 def test_full_size_sampled(w, count):
     note(f"{w.name}: GPU on the whole batch, oracle on {count} sampled sequences")
     W, pr = predictor(w.shape, w.weight_seed)

@@ -280,3 +280,69 @@ def test_tiny_workload_runs():
     pred, hid = oracle.oracle_forward(b.token_ids, b.cu_seqlens, m, w.shape)
     assert pred.shape == (8,) and np.all(np.isfinite(pred))
     assert hid.shape == (b.total, 128) and np.all(np.isfinite(hid))
+
+
+# ------------------------------------------------------------------------------ deep heads (Sec. 3.2, Sec. 4.2)
+def _deep_head(nl, hh, d, act, rng, nonneg=False):
+    shape = EncoderShape("h", 0, d, 1, 64, 10, 8, POOL_CLS, hh, True, head_layers=nl, head_act=act)
+    draw = (lambda *s: np.abs(rng.standard_normal(s))) if nonneg else (lambda *s: rng.standard_normal(s))
+    m = {"head_w1": draw(hh, d) / math.sqrt(d), "head_b1": draw(hh) * 0.1,
+         "head_mid_w": [draw(hh, hh) / math.sqrt(hh) for _ in range(nl - 2)],
+         "head_mid_b": [draw(hh) * 0.1 for _ in range(nl - 2)],
+         "head_w2": draw(1, hh) / math.sqrt(hh), "head_b2": draw(1) * 0.1}
+    return shape, m
+
+
+@pytest.mark.parametrize("act,nonneg", [(1, False), (0, True)])
+def test_deep_head_equals_composed_affine_map(act, nonneg):
+    """Eight linear layers collapse to one affine map W z + c (W = W8 ... W1); with ReLU
+    the same holds when weights, biases and input are all non-negative."""
+    rng = np.random.default_rng(11 + act)
+    d, hh = 24, 16
+    shape, m = _deep_head(8, hh, d, act, rng, nonneg)
+    Ws = [m["head_w1"]] + m["head_mid_w"] + [m["head_w2"]]
+    bs = [m["head_b1"]] + m["head_mid_b"] + [m["head_b2"]]
+    W, c = np.eye(d), np.zeros(d)
+    for w, b in zip(Ws, bs):
+        W, c = w @ W, w @ c + b
+    for _ in range(5):
+        z = np.abs(rng.standard_normal(d)) if nonneg else rng.standard_normal(d)
+        y = float((W @ z + c)[0])
+        assert abs(oracle.regression_head(z, m, shape) - (shape.out_shift + shape.out_scale * y)) < 1e-9
+
+
+def test_deep_head_matches_torch_sequential():
+    rng = np.random.default_rng(5)
+    d, hh = 32, 24
+    shape, m = _deep_head(8, hh, d, 0, rng)
+    Ws = [m["head_w1"]] + m["head_mid_w"] + [m["head_w2"]]
+    bs = [m["head_b1"]] + m["head_mid_b"] + [m["head_b2"]]
+    mods = []
+    for i, (w, b) in enumerate(zip(Ws, bs)):
+        lin = torch.nn.Linear(w.shape[1], w.shape[0], dtype=torch.float64)
+        with torch.no_grad():
+            lin.weight.copy_(torch.from_numpy(w))
+            lin.bias.copy_(torch.from_numpy(np.asarray(b)))
+        mods.append(lin)
+        if i < len(Ws) - 1:
+            mods.append(torch.nn.ReLU())
+    net = torch.nn.Sequential(*mods)
+    for _ in range(5):
+        z = rng.standard_normal(d)
+        y = float(net(torch.from_numpy(z)).item())
+        assert abs(oracle.regression_head(z, m, shape) - (shape.out_shift + shape.out_scale * y)) < 1e-9
+
+
+def test_deep_head_workload_weights():
+    from workloads import TINY_HEAD8, BERT_BASE_HEAD8, TINY_CLS_LIN8
+    for shape in (TINY_HEAD8, TINY_CLS_LIN8):
+        W = make_weights(shape, 1)
+        assert shape.n_head_layers == 8
+        assert len(W.master["head_mid_w"]) == 6 and len(W.device["head_mid_b"]) == 6
+        assert W.master["head_w1"].shape == (shape.head_hidden, shape.d_model)
+        assert W.master["head_mid_w"][0].shape == (shape.head_hidden, shape.head_hidden)
+        assert W.master["head_w2"].shape == (1, shape.head_hidden)
+    assert BERT_BASE_HEAD8.n_head_layers == 8 and BERT_BASE_HEAD8.head_hidden == 1024
+    assert BERT_BASE_HEAD8.pooling == POOL_MEAN
+    # the one- and two-layer heads keep their shapes
+    assert TINY.n_head_layers == 1

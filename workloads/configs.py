@@ -14,6 +14,8 @@ from dataclasses import dataclass, field
 
 POOL_CLS = 0
 POOL_MEAN = 1
+ACT_RELU = 0
+ACT_IDENTITY = 1
 
 
 @dataclass(frozen=True)
@@ -26,20 +28,36 @@ class EncoderShape:
     vocab: int
     max_pos: int
     pooling: int            # POOL_CLS or POOL_MEAN
-    head_hidden: int        # 0: linear d->1; else d->head_hidden->ReLU->1
+    head_hidden: int        # width of the head's hidden layers; 0: one linear layer d->1
     fp32_master: bool       # True: weights drawn and kept in fp32 (device gets bf16 copies)
     ln_eps: float = 1e-12
     out_scale: float = 100.0
     out_shift: float = 250.0
+    head_layers: int = 0    # FC layers of the head; 0: 1 when head_hidden == 0, else 2
+    head_act: int = ACT_RELU  # activation between the head's layers
 
     @property
     def d_head(self) -> int:
         return self.d_model // self.n_heads
 
+    @property
+    def n_head_layers(self) -> int:
+        if self.head_layers:
+            return self.head_layers
+        return 2 if self.head_hidden else 1
+
 
 TINY = EncoderShape("tiny", 2, 128, 4, 512, 1000, 128, POOL_CLS, 0, True)
 BERT_BASE = EncoderShape("bert_base", 12, 768, 12, 3072, 30522, 512, POOL_CLS, 256, False)
 XLMR_LARGE = EncoderShape("xlmr_large", 24, 1024, 16, 4096, 250002, 2048, POOL_MEAN, 0, False)
+# The paper's predictor heads: eight FC layers of width 1024 with ReLU on mean pooling (Sec. 4.2),
+# and eight linear layers on the CLS vector (Sec. 3.2, hidden width not stated: 1024 taken);
+# tiny versions of both for full-batch parity.
+BERT_BASE_HEAD8 = EncoderShape("bert_base_head8", 12, 768, 12, 3072, 30522, 512, POOL_MEAN, 1024, False,
+                               head_layers=8)
+TINY_HEAD8 = EncoderShape("tiny_head8", 2, 128, 4, 512, 1000, 128, POOL_MEAN, 64, True, head_layers=8)
+TINY_CLS_LIN8 = EncoderShape("tiny_cls_lin8", 2, 128, 4, 512, 1000, 128, POOL_CLS, 64, True, head_layers=8,
+                             head_act=ACT_IDENTITY)
 
 
 @dataclass(frozen=True)
@@ -82,6 +100,13 @@ W_BERT_B64 = Workload("bert_base_b64", BERT_BASE, n_seqs=64, batch_cap=32, len_k
 W_BERT_B256_ROUNDS = Workload("bert_base_b256_x100", BERT_BASE, n_seqs=256, batch_cap=128,
                               len_kind="prompt+gen", prompt_median=200.0, prompt_sigma=0.8,
                               gen_hi=300, max_len=512, rounds=100, data_seed=3, weight_seed=1002)
+W_TINY_HEAD8 = Workload("tiny_head8_b8", TINY_HEAD8, n_seqs=8, batch_cap=4, len_kind="uniform",
+                        len_lo=16, len_hi=64, data_seed=1, weight_seed=1005)
+W_TINY_CLS_LIN8 = Workload("tiny_cls_lin8_b8", TINY_CLS_LIN8, n_seqs=8, batch_cap=4, len_kind="uniform",
+                           len_lo=16, len_hi=64, data_seed=1, weight_seed=1007)
+W_BERT_B64_HEAD8 = Workload("bert_base_head8_b64", BERT_BASE_HEAD8, n_seqs=64, batch_cap=32,
+                            len_kind="prompt+gen", prompt_median=200.0, prompt_sigma=0.8, gen_hi=300,
+                            max_len=512, data_seed=2, weight_seed=1006)
 W_XLMR_B128 = Workload("xlmr_large_b128", XLMR_LARGE, n_seqs=128, batch_cap=64, len_kind="lognormal",
                        id_kind="zipf", len_median=600.0, len_sigma=0.9, max_len=2048,
                        data_seed=4, weight_seed=1004)
@@ -108,5 +133,6 @@ class RequestStream:
 
 S_ISRTF = RequestStream("isrtf_sim_4096", BERT_BASE)
 
-WORKLOADS = {w.name: w for w in (W_TINY, W_BERT_B64, W_BERT_B256_ROUNDS, W_XLMR_B128)}
-SHAPES = {s.name: s for s in (TINY, BERT_BASE, XLMR_LARGE)}
+WORKLOADS = {w.name: w for w in (W_TINY, W_BERT_B64, W_BERT_B256_ROUNDS, W_XLMR_B128, W_TINY_HEAD8,
+                                  W_TINY_CLS_LIN8, W_BERT_B64_HEAD8)}
+SHAPES = {s.name: s for s in (TINY, BERT_BASE, XLMR_LARGE, TINY_HEAD8, TINY_CLS_LIN8, BERT_BASE_HEAD8)}

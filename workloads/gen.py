@@ -10,6 +10,8 @@ Generator: numpy PCG64 throughout. ``lognormal(m, s)`` means
 Weight recipe (N(0, 0.02) everywhere, with LayerNorm gains centred on 1):
   matrices, embedding tables, biases, head:  N(0, 0.02)
   LayerNorm gain: 1 + N(0, 0.02); LayerNorm bias: N(0, 0.02)
+  heads of more than two layers: matrices N(0, 2 / fan_in) (He), biases N(0, 0.02),
+    so that a random deep head neither vanishes nor explodes
 Matrices and embedding tables of the bf16 shapes are drawn in fp32 and rounded
 to bf16 with round-to-nearest-even; the exact bf16 values are the weights of
 record. The tiny shape keeps fp32 master weights; its device copy is the bf16
@@ -99,12 +101,22 @@ def make_weights(shape: EncoderShape, seed: int) -> Weights:
         m["b_2"].append(_normal(rng, (d,)))
         m["ln2_g"].append(1.0 + _normal(rng, (d,)))
         m["ln2_b"].append(_normal(rng, (d,)))
-    if shape.head_hidden:
-        m["head_w1"] = _normal(rng, (shape.head_hidden, d))
-        m["head_b1"] = _normal(rng, (shape.head_hidden,))
-        m["head_w2"] = _normal(rng, (1, shape.head_hidden))
-    else:
+    nh, hh = shape.n_head_layers, shape.head_hidden
+    if nh == 1:
         m["head_w2"] = _normal(rng, (1, d))
+    elif nh == 2:
+        m["head_w1"] = _normal(rng, (hh, d))
+        m["head_b1"] = _normal(rng, (hh,))
+        m["head_w2"] = _normal(rng, (1, hh))
+    else:
+        he = lambda shp: _normal(rng, shp, std=math.sqrt(2.0 / shp[1]))
+        m["head_w1"] = he((hh, d))
+        m["head_b1"] = _normal(rng, (hh,))
+        m["head_mid_w"], m["head_mid_b"] = [], []
+        for _ in range(nh - 2):
+            m["head_mid_w"].append(he((hh, hh)))
+            m["head_mid_b"].append(_normal(rng, (hh,)))
+        m["head_w2"] = he((1, hh))
     m["head_b2"] = _normal(rng, (1,))
 
     dev: dict = {}
