@@ -413,6 +413,136 @@ def isrtf_rounds(max_rounds=None):
     print(json.dumps({"isrtf_rounds": out}), flush=True)
 
 
+POLICY_PROFILE = os.path.join(ROOT, "profiles", "policy_study.md")
+
+
+def policy_study():
+    """Synthetic analogue of the paper's scheduler comparison (Fig. 5 and 6): FCFS, ISRTF and SJF
+    on the device job table (keys cached in HBM, selection by elis_jobs_select[_aged]), 200
+    requests with Gamma(0.73) intervals, batch caps 1/2/4 at 1x/3x/5x the average request rate,
+    3 shuffled repetitions each. ISRTF's keys come from a stand-in predictor with the paper's
+    final MAE (true remaining + Laplace noise); starvation control (aging) and re-prefill cost
+    are measured at batch 4; one ISRTF run per rate uses the BERT-base-shaped encoder on the GPU
+    (random weights: its predictions carry no length information)."""
+    import numpy as np
+    import torch
+
+    from paper_2505_09142_amd.device import DeviceWeights, Predictor
+    from paper_2505_09142_amd.driver import DeviceRoundDriver
+    from paper_2505_09142_amd.scheduler import run_schedule
+    from workloads import BERT_BASE, POLICY_STUDY, accuracy_model_keys, make_policy_requests, make_weights
+    st = POLICY_STUDY
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    runs = []
+
+    def one(policy, cap, rps, rep, aging=0.0, prefill=0.0, encoder=None):
+        req = make_policy_requests(st, cap, rps, rep)
+        rem = np.array([len(r) for r in req.response])
+
+        def key_fn(jobs, gen):
+            jobs = np.asarray(jobs)
+            return accuracy_model_keys(st.data_seed, jobs, gen[jobs], rem[jobs] - gen[jobs], st.accuracy_mae)
+        drv = DeviceRoundDriver(encoder, 256, BERT_BASE.max_pos, dev)
+        res = run_schedule(req.arrival_t, req.prompt, req.response, drv, window=st.window,
+                           step_cost=st.step_cost_s, batch_cap=cap, policy=policy,
+                           key_fn=key_fn if (policy == "isrtf" and encoder is None) else None,
+                           aging=aging, prefill_cost=prefill)
+        lat = np.array([r.latency_s for r in res.rounds]) * 1e3
+        name = policy + ("_encoder" if encoder is not None else "") + (f"_aging{aging:g}" if aging else "") + \
+            (f"_prefill{prefill:g}" if prefill else "")
+        runs.append({"variant": name, "batch_cap": cap, "rps_multiple": rps, "repetition": rep,
+                     "mean_jct_s": float(res.jct.mean()), "mean_queue_s": float(res.queue_delay.mean()),
+                     "p99_jct_s": float(np.percentile(res.jct, 99)), "max_jct_s": float(res.jct.max()),
+                     "preemptions": int(res.preemptions.sum()), "rounds": len(res.rounds),
+                     "round_p50_ms": float(np.median(lat))})
+        t, bits = drv.table.status()
+        if t != 0:
+            raise SystemExit(f"job table status {t} bits {bits}")
+
+    for cap in st.batch_caps:
+        for rps in st.rps_multiples:
+            for rep in range(st.repetitions):
+                for policy in ("fcfs", "isrtf", "sjf"):
+                    one(policy, cap, rps, rep)
+                if cap == max(st.batch_caps):
+                    one("isrtf", cap, rps, rep, aging=st.aging)
+                    one("isrtf", cap, rps, rep, prefill=st.prefill_cost_s)
+                    one("isrtf", cap, rps, rep, aging=st.aging, prefill=st.prefill_cost_s)
+            print(f"policy study: batch {cap}, {rps:g}x done", file=sys.stderr, flush=True)
+    W = make_weights(BERT_BASE, 1002)
+    pr = Predictor(DeviceWeights(BERT_BASE, W.device, dev), dev)
+    cap = max(st.batch_caps)
+    for rps in st.rps_multiples:
+        one("isrtf", cap, rps, 0, encoder=pr)
+    print("policy study: encoder runs done", file=sys.stderr, flush=True)
+    print(json.dumps({"policy_study": {"requests": st.n_requests, "window": st.window,
+                                       "step_cost_s": st.step_cost_s, "gamma_shape": st.gamma_shape,
+                                       "accuracy_mae": st.accuracy_mae, "aging": st.aging,
+                                       "prefill_cost_s": st.prefill_cost_s, "runs": runs}}), flush=True)
+
+
+def summarize_policy(study_json, command):
+    """Write the policy-study summary (mean over repetitions) from bench.py --policy-study's line."""
+    import collections
+    rec = json.loads(open(study_json).read().strip().splitlines()[-1])["policy_study"]
+    agg = collections.defaultdict(list)
+    for r in rec["runs"]:
+        agg[(r["variant"], r["batch_cap"], r["rps_multiple"])].append(r)
+    mean = {k: {f: sum(x[f] for x in v) / len(v) for f in ("mean_jct_s", "mean_queue_s", "p99_jct_s",
+                                                          "preemptions", "rounds", "round_p50_ms")}
+            for k, v in agg.items()}
+    variants = sorted({k[0] for k in mean}, key=lambda v: (v != "fcfs", v != "isrtf", v != "sjf", v))
+    caps = sorted({k[1] for k in mean})
+    rpss = sorted({k[2] for k in mean})
+    lines = ["# Scheduler policy study (synthetic analogue of Fig. 5 and 6)", "",
+             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             f"{rec['requests']} synthetic requests per run (prompt lognormal(200, 0.8), response lognormal(250, 1.0) "
+             f"capped at 2048), Gamma(shape {rec['gamma_shape']}) request intervals at k x batch / (mean response "
+             f"length x {rec['step_cost_s'] * 1e3:g} ms per decode step) requests/s, {rec['window']}-token windows, "
+             "the same request set shuffled for each of 3 repetitions (means below). Every run is the scheduling "
+             "loop on the device job table: keys cached in HBM, batches chosen by `elis_jobs_select` / "
+             "`elis_jobs_select_aged`; the same trajectories are reproduced exactly by the oracle simulator in "
+             "`tests/test_gpu_policies.py`.", "",
+             f"ISRTF keys: a stand-in predictor with the paper's final MAE ({rec['accuracy_mae']} tokens): true "
+             "remaining length + Laplace noise. `isrtf_encoder`: the BERT-base-shaped encoder on the GPU with random "
+             "weights (no length information, so it ranks jobs arbitrarily). Aging: "
+             f"{rec['aging']:g} tokens per second of waiting; re-prefill cost {rec['prefill_cost_s'] * 1e3:g} ms "
+             "per token for a preempted job that resumes.", "",
+             "## Mean JCT (s) and improvement over FCFS", "",
+             "| batch | rate | " + " | ".join(variants) + " |", "|---|---|" + "---:|" * len(variants)]
+    for cap in caps:
+        for rps in rpss:
+            base = mean.get(("fcfs", cap, rps))
+            cells = []
+            for v in variants:
+                m = mean.get((v, cap, rps))
+                if m is None:
+                    cells.append("")
+                elif v == "fcfs" or base is None:
+                    cells.append(f"{m['mean_jct_s']:.2f}")
+                else:
+                    cells.append(f"{m['mean_jct_s']:.2f} ({100 * (1 - m['mean_jct_s'] / base['mean_jct_s']):+.1f}%)")
+            lines.append(f"| {cap} | {rps:g}x | " + " | ".join(cells) + " |")
+    lines += ["", "## Mean queuing delay (s), preemptions per run, scheduling rounds per run", "",
+              "| variant | batch | rate | queuing delay | p99 JCT | preemptions | rounds | p50 round ms |",
+              "|---|---|---|---:|---:|---:|---:|---:|"]
+    for v in variants:
+        for cap in caps:
+            for rps in rpss:
+                m = mean.get((v, cap, rps))
+                if m is None:
+                    continue
+                lines.append(f"| {v} | {cap} | {rps:g}x | {m['mean_queue_s']:.2f} | {m['p99_jct_s']:.2f} | "
+                             f"{m['preemptions']:.0f} | {m['rounds']:.0f} | {m['round_p50_ms']:.3f} |")
+    lines += ["", "Round latency: host wall time of one round's key update plus selection on the device, "
+              "including the host-to-device upload of the candidates and the read-back of the chosen jobs "
+              "(the encoder variant includes the predictor pass)."]
+    with open(POLICY_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {POLICY_PROFILE}")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -430,6 +560,10 @@ def main():
                     help="write the ISRTF round-latency summary")
     ap.add_argument("--isrtf-rounds", action="store_true",
                     help="per-round latency of the ISRTF loop: device job table vs host packing")
+    ap.add_argument("--policy-study", action="store_true",
+                    help="FCFS / ISRTF / SJF, aging and re-prefill cost on the device job table (Fig. 5/6 analogue)")
+    ap.add_argument("--summarize-policy", nargs=2, metavar=("STUDY_JSON", "COMMAND"),
+                    help="write the policy-study summary")
     ap.add_argument("--select-sweep", action="store_true",
                     help="time the device-wide select at n = 2^20 .. 2^24 instead of the step")
     ap.add_argument("--summarize-select", nargs=3, metavar=("SWEEP_JSON", "TRACE_CSV", "COMMAND"),
@@ -444,6 +578,12 @@ def main():
         return
     if args.isrtf_rounds:
         isrtf_rounds()
+        return
+    if args.policy_study:
+        policy_study()
+        return
+    if args.summarize_policy:
+        summarize_policy(*args.summarize_policy)
         return
     if args.summarize_select:
         summarize_select(*args.summarize_select)

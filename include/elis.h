@@ -253,6 +253,23 @@ size_t elis_jobs_select_workspace_bytes(int32_t a);
 int elis_jobs_select(const elis_job_table *t, const int32_t *slots, int32_t a, int32_t batch_cap,
                      int32_t *out_slots, int32_t *out_count, void *workspace, size_t ws_bytes, void *stream);
 
+/*
+ * The same select with aged keys, a starvation control (Sec. 3.4: the
+ * frequency of preemption is tunable; the paper gives no formula, this is the
+ * library's): candidate i is ranked by
+ *     key_i = fl32( fl64(pred[slot_i]) - fl64(aging) * fl64(wait[i]) )
+ * evaluated in IEEE fp64 with the product and the difference each rounded
+ * (no fused multiply-add) and one final rounding to fp32; ties as
+ * elis_isrtf_select. wait (device fp32 [a]) is the time candidate i has
+ * waited since it last ran or arrived, in the caller's unit (seconds in the
+ * package's loop); aging is the key reduction per unit of waiting (tokens per
+ * second), finite (else ELIS_EINVAL). aging = 0 ranks exactly like
+ * elis_jobs_select. Other arguments, limits and errors as elis_jobs_select.
+ */
+int elis_jobs_select_aged(const elis_job_table *t, const int32_t *slots, const float *wait, float aging, int32_t a,
+                          int32_t batch_cap, int32_t *out_slots, int32_t *out_count, void *workspace,
+                          size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------ building blocks
  * The predictor's kernels, exposed one by one for per-kernel parity tests and
  * measurement. Same conventions as above.

@@ -12,4 +12,4 @@ from .encoder import (POOL_CLS, POOL_MEAN, embed, encode_sequence, encoder_layer
                       layer_norm, oracle_forward, pool, regression_head, self_attention,
                       softmax_rows)
 from .select import oracle_order, oracle_select
-from .simulate import SimResult, job_input, simulate
+from .simulate import POLICIES, SimResult, aged_keys, job_input, simulate

@@ -106,6 +106,8 @@ SIGNATURES = {
     "elis_jobs_select_workspace_bytes": (c_size_t, [c_int32]),
     "elis_jobs_select": (c_int, [POINTER(elis_job_table), c_void_p, c_int32, c_int32, c_void_p, c_void_p,
                                  c_void_p, c_size_t, c_void_p]),
+    "elis_jobs_select_aged": (c_int, [POINTER(elis_job_table), c_void_p, c_void_p, c_float, c_int32, c_int32,
+                                      c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "elis_timing_enable": (c_int, [c_uint32]),
     "elis_timing_reset": (c_int, []),
     "elis_timing_read": (c_int, [c_int32, POINTER(c_int32), POINTER(c_double)]),
@@ -229,6 +231,13 @@ def elis_jobs_select_workspace_bytes(a: int) -> int:
 def elis_jobs_select(t: elis_job_table, slots: int, a: int, batch_cap: int, out_slots: int | None, out_count: int,
                      workspace: int, ws_bytes: int, stream: int | None) -> int:
     return lib().elis_jobs_select(_tab(t), slots, a, batch_cap, out_slots, out_count, workspace, ws_bytes, stream)
+
+
+def elis_jobs_select_aged(t: elis_job_table, slots: int, wait: int, aging: float, a: int, batch_cap: int,
+                          out_slots: int | None, out_count: int, workspace: int, ws_bytes: int,
+                          stream: int | None) -> int:
+    return lib().elis_jobs_select_aged(_tab(t), slots, wait, aging, a, batch_cap, out_slots, out_count, workspace,
+                                       ws_bytes, stream)
 
 
 def elis_timing_enable(class_mask: int) -> int:

@@ -367,8 +367,11 @@ size_t elis_jobs_select_workspace_bytes(int32_t a) {
     return jobs_select_workspace_bytes(a);
 }
 
-int elis_jobs_select(const elis_job_table* t, const int32_t* slots, int32_t a, int32_t batch_cap,
-                     int32_t* out_slots, int32_t* out_count, void* workspace, size_t ws_bytes, void* stream) {
+namespace {
+
+int jobs_select_common(const elis_job_table* t, const int32_t* slots, const float* wait, float aging, int32_t a,
+                       int32_t batch_cap, int32_t* out_slots, int32_t* out_count, void* workspace, size_t ws_bytes,
+                       void* stream) {
     int r = check_table(t);
     if (r != ELIS_OK) return r;
     if (!slots || !out_count || !workspace || (batch_cap > 0 && !out_slots)) return ELIS_EINVAL;
@@ -379,9 +382,25 @@ int elis_jobs_select(const elis_job_table* t, const int32_t* slots, int32_t a, i
     if (ws_bytes < jobs_select_workspace_bytes(a)) return ELIS_EWORKSPACE;
     hipStream_t st = static_cast<hipStream_t>(stream);
     return status_of(timed(ELIS_K_SELECT, st, [&] {
-        return launch_jobs_select(jobs_table(t->base, t->max_jobs, t->max_pos), slots, a, batch_cap, out_slots,
-                                  out_count, workspace, st);
+        return launch_jobs_select(jobs_table(t->base, t->max_jobs, t->max_pos), slots, wait, aging, a, batch_cap,
+                                  out_slots, out_count, workspace, st);
     }));
+}
+
+}  // namespace
+
+int elis_jobs_select(const elis_job_table* t, const int32_t* slots, int32_t a, int32_t batch_cap,
+                     int32_t* out_slots, int32_t* out_count, void* workspace, size_t ws_bytes, void* stream) {
+    return jobs_select_common(t, slots, nullptr, 0.f, a, batch_cap, out_slots, out_count, workspace, ws_bytes,
+                              stream);
+}
+
+int elis_jobs_select_aged(const elis_job_table* t, const int32_t* slots, const float* wait, float aging, int32_t a,
+                          int32_t batch_cap, int32_t* out_slots, int32_t* out_count, void* workspace,
+                          size_t ws_bytes, void* stream) {
+    if (!wait || !isfinite(aging)) return ELIS_EINVAL;
+    return jobs_select_common(t, slots, wait, aging, a, batch_cap, out_slots, out_count, workspace, ws_bytes,
+                              stream);
 }
 
 int elis_read_status(const void* workspace, void* stream, uint32_t* bits) {

@@ -164,7 +164,12 @@ __global__ __launch_bounds__(kThreads) void jobs_store_pred_kernel(JobTable t, c
     t.pred[s] = pred[i];
 }
 
+// Gathers the select keys of the active jobs. With `wait` (seconds each job has waited since
+// it last ran, fp32), the key is aged: fl32(key - aging * wait) evaluated in fp64 from the fp32
+// operands, with the product and the difference each rounded once (no fused multiply-add), so
+// the rank order is reproducible exactly in any IEEE fp64 arithmetic.
 __global__ __launch_bounds__(kThreads) void jobs_gather_kernel(JobTable t, const int32_t* __restrict__ slots, int a,
+                                                               const float* __restrict__ wait, float aging,
                                                                float* __restrict__ pred, int64_t* __restrict__ arr,
                                                                uint32_t* __restrict__ status) {
     const int i = blockIdx.x * kThreads + threadIdx.x;
@@ -176,7 +181,10 @@ __global__ __launch_bounds__(kThreads) void jobs_gather_kernel(JobTable t, const
         arr[i] = 0;
         return;
     }
-    pred[i] = t.pred[s];
+    float key = t.pred[s];
+    if (wait) key = __double2float_rn(__dsub_rn(static_cast<double>(key),
+                                                __dmul_rn(static_cast<double>(aging), static_cast<double>(wait[i]))));
+    pred[i] = key;
     arr[i] = t.arrival[s];
 }
 
@@ -258,8 +266,8 @@ size_t jobs_select_workspace_bytes(int max_active) {
     return align_up(4 * a) + align_up(8 * a) + align_up(4 * a) + sel;
 }
 
-hipError_t launch_jobs_select(JobTable t, const int32_t* slots, int a, int k, int32_t* out_slots, int32_t* out_count,
-                              void* workspace, hipStream_t st) {
+hipError_t launch_jobs_select(JobTable t, const int32_t* slots, const float* wait, float aging, int a, int k,
+                              int32_t* out_slots, int32_t* out_count, void* workspace, hipStream_t st) {
     const size_t n = static_cast<size_t>(a);
     char* p = static_cast<char*>(workspace);
     float* pred = reinterpret_cast<float*>(p);
@@ -267,7 +275,8 @@ hipError_t launch_jobs_select(JobTable t, const int32_t* slots, int a, int k, in
     int32_t* idx = reinterpret_cast<int32_t*>(p + align_up(4 * n) + align_up(8 * n));
     void* sel_ws = p + align_up(4 * n) + align_up(8 * n) + align_up(4 * n);
     // Bad slots are flagged in the table's status word: the select clears its own.
-    hipLaunchKernelGGL(jobs_gather_kernel, grid_for(a), dim3(kThreads), 0, st, t, slots, a, pred, arr, t.status);
+    hipLaunchKernelGGL(jobs_gather_kernel, grid_for(a), dim3(kThreads), 0, st, t, slots, a, wait, aging, pred, arr,
+                       t.status);
     hipError_t e = launch_select(pred, arr, a, k, idx, out_count, sel_ws, st);
     if (e != hipSuccess) return e;
     const int kk = k < a ? k : a;

@@ -102,7 +102,8 @@ hipError_t launch_jobs_pack(JobTable t, const int32_t* slots, int n, int total, 
                             int32_t* cu, hipStream_t st);
 hipError_t launch_jobs_store_pred(JobTable t, const int32_t* slots, const float* pred, int n, hipStream_t st);
 size_t jobs_select_workspace_bytes(int max_active);
-hipError_t launch_jobs_select(JobTable t, const int32_t* slots, int a, int k, int32_t* out_slots, int32_t* out_count,
-                              void* workspace, hipStream_t st);
+// wait: null, or fp32 [a] seconds waited, aging the keys by `aging` tokens per second.
+hipError_t launch_jobs_select(JobTable t, const int32_t* slots, const float* wait, float aging, int a, int k,
+                              int32_t* out_slots, int32_t* out_count, void* workspace, hipStream_t st);
 
 }  // namespace elis

@@ -171,11 +171,18 @@ class JobTable:
                 "elis_jobs_store_pred")
 
     def select(self, slots: torch.Tensor, batch_cap: int, out_slots: torch.Tensor, out_count: torch.Tensor,
-               stream=None):
+               stream=None, wait: torch.Tensor | None = None, aging: float = 0.0):
+        """Select over the cached keys; with `wait` (fp32 seconds per candidate) the keys are aged by
+        `aging` tokens per second (elis_jobs_select_aged)."""
         a = slots.numel()
         ws, wsb = self.sel_ws.get(E.elis_jobs_select_workspace_bytes(a))
-        E.check(E.elis_jobs_select(self.t, slots.data_ptr(), a, batch_cap, out_slots.data_ptr(), out_count.data_ptr(),
-                                   ws, wsb, _stream(stream)), "elis_jobs_select")
+        if wait is None:
+            E.check(E.elis_jobs_select(self.t, slots.data_ptr(), a, batch_cap, out_slots.data_ptr(),
+                                       out_count.data_ptr(), ws, wsb, _stream(stream)), "elis_jobs_select")
+        else:
+            E.check(E.elis_jobs_select_aged(self.t, slots.data_ptr(), wait.data_ptr(), aging, a, batch_cap,
+                                            out_slots.data_ptr(), out_count.data_ptr(), ws, wsb, _stream(stream)),
+                    "elis_jobs_select_aged")
 
     def status(self, stream=None):
         return E.elis_read_status(self.t.base, _stream(stream))

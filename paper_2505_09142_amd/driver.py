@@ -145,7 +145,7 @@ class DeviceRoundDriver:
         """Concatenates int32 / int64 arrays into the pinned staging buffer, copies it to the
         device in one transfer, and returns device views of the parts (int64 parts viewed
         back as int64)."""
-        words = [np.ascontiguousarray(p).view(np.int32) if p.dtype == np.int64 else
+        words = [np.ascontiguousarray(p).view(np.int32) if p.dtype in (np.int64, np.float32) else
                  np.ascontiguousarray(p, dtype=np.int32) for p in parts]
         # int64 parts start on an even word so the view back is 8-byte aligned
         offs, n = [], 0
@@ -171,7 +171,8 @@ class DeviceRoundDriver:
         out = []
         for o, w, p in zip(offs, words, parts):
             v = self._d[o:o + len(w)]
-            out.append(v.view(torch.int64) if p.dtype == np.int64 else v)
+            out.append(v.view(torch.int64) if p.dtype == np.int64 else
+                       v.view(torch.float32) if p.dtype == np.float32 else v)
         return out
 
     def release(self, jobs):
@@ -237,13 +238,25 @@ class DeviceRoundDriver:
         self.table.store_pred(d_slots, pred)
         return pred
 
-    def select(self, candidates, batch_cap: int) -> np.ndarray:
-        """Chosen job ids among the candidates (cached predictions, ties by arrival number)."""
+    def store_keys(self, jobs, keys) -> None:
+        """Caches priority keys computed outside the encoder (FCFS, SJF, a stand-in predictor)."""
+        d_slots, d_keys = self._upload(np.fromiter((self.slot_of[j] for j in jobs), dtype=np.int32, count=len(jobs)),
+                                       np.asarray(keys, dtype=np.float32))
+        self.table.store_pred(d_slots, d_keys)
+
+    def select(self, candidates, batch_cap: int, wait=None, aging: float = 0.0) -> np.ndarray:
+        """Chosen job ids among the candidates (cached keys, ties by arrival number); with `wait`
+        (fp32 seconds per candidate) the keys are aged on the device by `aging` per second."""
         n = len(candidates)
-        (d_slots,) = self._upload(np.fromiter((self.slot_of[j] for j in candidates), dtype=np.int32, count=n))
+        slots = np.fromiter((self.slot_of[j] for j in candidates), dtype=np.int32, count=n)
+        if wait is None:
+            (d_slots,) = self._upload(slots)
+            d_wait = None
+        else:
+            d_slots, d_wait = self._upload(slots, np.asarray(wait, dtype=np.float32))
         if self._out_slots.numel() < max(1, batch_cap):
             self._out_slots = torch.empty(max(1, batch_cap), dtype=torch.int32, device=self.device)
-        self.table.select(d_slots, batch_cap, self._out_slots, self._out_count)
+        self.table.select(d_slots, batch_cap, self._out_slots, self._out_count, wait=d_wait, aging=aging)
         # one transfer back: the count and the chosen slots
         res = torch.cat([self._out_count, self._out_slots[:min(batch_cap, n)]]).cpu().numpy()
         self.d2h_bytes += 4 * len(res)
@@ -282,7 +295,12 @@ class HostRoundDriver:
         self.d2h_bytes += 4 * len(inputs)
         return pred
 
-    def select(self, candidates, batch_cap: int) -> np.ndarray:
+    def store_keys(self, jobs, keys) -> None:
+        self.pred[list(jobs)] = np.asarray(keys, dtype=np.float32)
+
+    def select(self, candidates, batch_cap: int, wait=None, aging: float = 0.0) -> np.ndarray:
+        if wait is not None:
+            raise NotImplementedError("aged keys need the device job table (DeviceRoundDriver)")
         cand = np.asarray(candidates, dtype=np.int64)
         local = self.rd.select(self.pred[cand], cand, batch_cap)
         self.h2d_bytes += 12 * len(cand)

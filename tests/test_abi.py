@@ -218,3 +218,11 @@ def test_job_table_rejects_invalid_arguments(lib):
     assert E.elis_jobs_select(good, FAKE, 100, -1, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
     big = E.elis_jobs_select_workspace_bytes(10000)
     assert E.elis_jobs_select(good, FAKE, 10000, 9000, FAKE, FAKE, FAKE_WS, big, None) == E.ELIS_EUNSUPPORTED
+    # aged select: same checks plus a missing wait array or a non-finite aging rate
+    assert E.elis_jobs_select_aged(good, FAKE, None, 1.0, 100, 4, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_select_aged(good, FAKE, FAKE, float("nan"), 100, 4, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_select_aged(good, FAKE, FAKE, float("inf"), 100, 4, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_select_aged(good, FAKE, FAKE, 1.0, 100, 4, FAKE, FAKE, FAKE_WS, ws - 1, None) == E.ELIS_EWORKSPACE
+    assert E.elis_jobs_select_aged(good, FAKE, FAKE, 1.0, 0, 4, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
+    assert E.elis_jobs_select_aged(good, FAKE, FAKE, 1.0, 10000, 9000, FAKE, FAKE, FAKE_WS, big, None) == \
+        E.ELIS_EUNSUPPORTED

@@ -15,7 +15,7 @@ import itertools
 import numpy as np
 import pytest
 
-from oracle import job_input, simulate
+from oracle import aged_keys, job_input, simulate
 
 
 def _true_remaining(responses):
@@ -105,3 +105,109 @@ def test_job_input_truncation():
     assert job_input(prompt, resp, 3, 64).tolist() == [1, 2, 3, 4, 5, 100, 101, 102]
     # 15 tokens, keep the first and the last 5
     assert job_input(prompt, resp, 10, 6).tolist() == [1, 105, 106, 107, 108, 109]
+
+
+# ----------------------------------------------------------------------------- policies, aging, preemption cost
+
+def test_fcfs_policy_runs_in_arrival_order():
+    lengths = [7, 2, 11, 4, 9, 3]
+    prompts, responses = _jobs(lengths, 1)
+    c = 0.5
+    res = simulate(np.zeros(6), prompts, responses, window=50, step_cost=c, batch_cap=1, max_pos=64, policy="fcfs")
+    # one slot, every job fits one window: jobs finish back to back in arrival order
+    np.testing.assert_allclose(res.finish_t, np.cumsum(lengths) * c)
+    assert [rr.selected for rr in res.rounds] == [[j] for j in range(6)]
+
+
+@pytest.mark.parametrize("lengths", [[5, 2, 9, 1], [3, 3, 1, 7, 2], [4, 8, 1, 6, 2, 5]])
+def test_sjf_policy_is_optimal_for_simultaneous_arrivals(lengths):
+    prompts, responses = _jobs(lengths)
+    c = 0.01
+    res = simulate(np.zeros(len(lengths)), prompts, responses, window=3, step_cost=c, batch_cap=1, max_pos=64,
+                   policy="sjf")
+    best = min(np.mean(np.cumsum([lengths[i] for i in order]) * c)
+               for order in itertools.permutations(range(len(lengths))))
+    assert abs(np.mean(res.jct) - best) < 1e-9
+
+
+def test_aged_keys_rounding():
+    # exact cases: 100 - 500 * fl32(0.1) = 49.99999925..., which rounds to 50 in fp32
+    assert aged_keys(np.float32([100.0]), np.float32([0.1]), 500.0)[0] == np.float32(50.0)
+    # aging 0 leaves every key (and its sign of zero) unchanged
+    k = np.float32([-0.0, 0.0, 3.5, np.inf, -np.inf])
+    out = aged_keys(k, np.float32([1, 2, 3, 4, 5]), 0.0)
+    assert np.array_equal(out.view(np.uint32), k.view(np.uint32))
+    assert np.isnan(aged_keys(np.float32([np.nan]), np.float32([1.0]), 2.0)[0])
+    # an fp32 result that needs the fp64 intermediate: 2^24 + 1 is not an fp32 value
+    got = aged_keys(np.float32([16777216.0]), np.float32([1.0]), -1.0)[0]
+    assert got == np.float32(16777216.0)      # 16777217 rounds to even
+    assert aged_keys(np.float32([3e38]), np.float32([1e30]), -1e10)[0] == np.inf
+
+
+def test_aging_and_preemption_cost_hand_example():
+    """Two jobs at t = 0 with 3-token prompts; SJF keys A = 30, B = 20; windows of 10 tokens at
+    0.01 s per step; aging 500 tokens/s; re-prefill 0.001 s per token. Worked by hand:
+      t=0      keys A 30, B 20                     -> B runs 10 tokens, ends 0.1
+      t=0.1    A waited 0.1: 30 - 50 = -20; B 20   -> A runs (first run, free), B preempted
+      t=0.2    A 30; B waited 0.1: 20 - 50 = -30   -> B resumes: re-prefill 3 + 10 = 13 tokens
+                                                       (0.013 s), finishes at 0.2 + 0.013 + 0.1 = 0.313
+      t=0.313  A alone, preempted at 0.2           -> re-prefill 13 tokens, runs to 0.426
+      t=0.426  A (ran last, KV kept)               -> finishes at 0.526
+    """
+    prompts, responses = _jobs([30, 20], 6)
+    res = simulate(np.zeros(2), prompts, responses, window=10, step_cost=0.01, batch_cap=1, max_pos=64,
+                   policy="sjf", aging=500.0, prefill_cost=0.001)
+    assert [rr.selected for rr in res.rounds] == [[1], [0], [1], [0], [0]]
+    assert [rr.resumed for rr in res.rounds] == [[], [], [1], [0], []]
+    np.testing.assert_allclose([rr.t for rr in res.rounds], [0.0, 0.1, 0.2, 0.313, 0.426], atol=1e-12)
+    np.testing.assert_allclose(res.finish_t, [0.526, 0.313], atol=1e-12)
+    assert res.preemptions.tolist() == [1, 1]
+    np.testing.assert_allclose(res.queue_delay, [0.526 - 0.3, 0.313 - 0.2], atol=1e-12)
+    # without aging the short job runs to completion first and nothing is preempted
+    plain = simulate(np.zeros(2), prompts, responses, window=10, step_cost=0.01, batch_cap=1, max_pos=64,
+                     policy="sjf", prefill_cost=0.001)
+    assert [rr.selected for rr in plain.rounds] == [[1], [1], [0], [0], [0]]
+    assert plain.preemptions.tolist() == [0, 0]
+    np.testing.assert_allclose(plain.finish_t, [0.5, 0.2], atol=1e-12)
+
+
+@pytest.mark.parametrize("policy", ["fcfs", "sjf", "isrtf"])
+def test_conservation_with_aging_and_prefill(policy):
+    rng = np.random.default_rng(11)
+    lengths = rng.integers(1, 150, size=40)
+    prompts, responses = _jobs(lengths, 9)
+    arrival = np.sort(rng.uniform(0, 1.5, size=40))
+    c, cp = 0.01, 0.0005
+    res = simulate(arrival, prompts, responses, window=20, step_cost=c, batch_cap=3, max_pos=64, policy=policy,
+                   predict_fn=_true_remaining(responses), aging=30.0, prefill_cost=cp)
+    assert np.array_equal(res.generated, lengths)
+    assert np.all(res.queue_delay >= -1e-12)
+    # preemptions recounted from the trajectory: a job in one batch, unfinished, absent from the next
+    recount = np.zeros(len(lengths), dtype=np.int64)
+    for a, b in zip(res.rounds, res.rounds[1:]):
+        for j in a.selected:
+            if j in b.candidates and j not in b.selected:
+                recount[j] += 1
+    assert np.array_equal(recount, res.preemptions)
+    # every re-prefill is paid by a job preempted earlier, and costs at least its prompt
+    assert sum(len(rr.resumed) for rr in res.rounds) <= res.preemptions.sum()
+    for rr in res.rounds:
+        if rr.resumed:
+            assert rr.prefill_s >= cp * sum(len(prompts[j]) for j in rr.resumed) - 1e-15
+        else:
+            assert rr.prefill_s == 0.0
+    # the clock only moves by window lengths (and jumps to the next arrival when idle)
+    for a, b in zip(res.rounds, res.rounds[1:]):
+        assert b.t >= a.t + a.prefill_s + a.window_steps * c - 1e-12
+
+
+def test_aging_zero_equals_plain_select():
+    rng = np.random.default_rng(2)
+    lengths = rng.integers(5, 80, size=25)
+    prompts, responses = _jobs(lengths, 4)
+    arrival = np.sort(rng.uniform(0, 0.5, size=25))
+    a = simulate(arrival, prompts, responses, window=10, step_cost=0.01, batch_cap=2, max_pos=64, policy="sjf")
+    b = simulate(arrival, prompts, responses, window=10, step_cost=0.01, batch_cap=2, max_pos=64, policy="sjf",
+                 aging=0.0, prefill_cost=0.0)
+    assert [r.selected for r in a.rounds] == [r.selected for r in b.rounds]
+    assert np.array_equal(a.finish_t, b.finish_t)

@@ -77,3 +77,39 @@ def test_requests():
     assert 15 < rate < 25
     R = np.array([len(x) for x in r.response])
     assert R.max() <= 2048 and R.min() >= 1 and 150 < np.median(R) < 400
+
+
+def test_policy_study_streams():
+    from workloads import POLICY_STUDY as st, make_policy_requests
+    a = make_policy_requests(st, 4, 3.0, 1)
+    b = make_policy_requests(st, 4, 3.0, 1)
+    assert np.array_equal(a.arrival_t, b.arrival_t)
+    assert all(np.array_equal(x, y) for x, y in zip(a.response, b.response))
+    c = make_policy_requests(st, 4, 3.0, 2)
+    # the same request set in another order
+    key = lambda r: sorted(tuple(x[:4].tolist()) + (len(x),) for x in r.response)
+    assert key(a) == key(c) and not np.array_equal(a.arrival_t, c.arrival_t)
+    assert len(a) == st.n_requests and np.all(np.diff(a.arrival_t) >= 0)
+    # Gamma(0.73) intervals at the requested rate: mean 1 / rate, squared CV 1 / 0.73 (checked
+    # on a long draw of the same recipe)
+    rlen = np.array([len(x) for x in a.response])
+    rate = 3.0 * 4 / (rlen.mean() * st.step_cost_s)
+    rng = np.random.Generator(np.random.PCG64(0))
+    g = rng.gamma(st.gamma_shape, 1.0 / (rate * st.gamma_shape), size=400000)
+    assert abs(g.mean() * rate - 1) < 0.01 and abs(g.var() / g.mean() ** 2 - 1 / 0.73) < 0.03
+    gaps = np.diff(np.concatenate([[0.0], a.arrival_t]))
+    assert 0.5 < gaps.mean() * rate < 1.5
+
+
+def test_accuracy_model_keys():
+    from workloads import accuracy_model_keys
+    jobs = np.arange(200000)
+    k = accuracy_model_keys(3, jobs, np.zeros_like(jobs), np.full(jobs.shape, 100.0), 19.923)
+    err = k.astype(np.float64) - 100.0
+    assert abs(np.abs(err).mean() - 19.923) < 0.3          # Laplace(0, b): E|X| = b
+    assert abs(np.median(err)) < 0.3 and abs(err.var() - 2 * 19.923 ** 2) < 30
+    # a fixed function of (seed, job, generated): independent of batching
+    one = accuracy_model_keys(3, [17], [50], [42.0], 19.923)
+    many = accuracy_model_keys(3, [5, 17, 9], [0, 50, 7], [1.0, 42.0, 3.0], 19.923)
+    assert one[0] == many[1] and k.dtype == np.float32
+    assert accuracy_model_keys(4, [17], [50], [42.0], 19.923)[0] != one[0]

@@ -24,7 +24,7 @@ import math
 
 import numpy as np
 
-from .configs import POOL_CLS, EncoderShape, RequestStream, Workload
+from .configs import POOL_CLS, EncoderShape, PolicyStudy, RequestStream, Workload
 
 # Tensors that the device stores in bf16 (everything else is fp32).
 BF16_TENSORS = ("word", "pos", "w_qkv", "w_o", "w_1", "w_2")
@@ -294,6 +294,52 @@ def make_requests(s: RequestStream, n: int | None = None, seed: int | None = Non
     prompt = [rng.integers(1, V, size=int(p)).astype(np.int32) for p in plen]
     response = [rng.integers(1, V, size=int(r)).astype(np.int32) for r in rlen]
     return Requests(arrival_t, prompt, response)
+
+
+def make_policy_requests(st: PolicyStudy, batch_cap: int, rps_multiple: float, repetition: int) -> Requests:
+    """One run of the policy study: the study's fixed request set, shuffled for this repetition,
+    with Gamma(shape, scale) request intervals at rps_multiple x batch_cap / (mean(R) x step_cost)
+    requests per second."""
+    base = np.random.Generator(np.random.PCG64(st.data_seed))
+    N = st.n_requests
+    plen = _lognormal_int(base, st.prompt_median, st.prompt_sigma, N)
+    rlen = np.minimum(st.resp_cap, _lognormal_int(base, st.resp_median, st.resp_sigma, N))
+    prompt = [base.integers(1, st.vocab, size=int(p)).astype(np.int32) for p in plen]
+    response = [base.integers(1, st.vocab, size=int(r)).astype(np.int32) for r in rlen]
+    rng = np.random.Generator(np.random.PCG64([st.data_seed, repetition, batch_cap, int(round(rps_multiple * 1000))]))
+    order = rng.permutation(N)
+    rate = rps_multiple * batch_cap / (float(rlen.mean()) * st.step_cost_s)
+    gaps = rng.gamma(st.gamma_shape, 1.0 / (rate * st.gamma_shape), size=N)
+    return Requests(np.cumsum(gaps), [prompt[i] for i in order], [response[i] for i in order])
+
+
+_M64 = (1 << 64) - 1
+
+
+def _splitmix64(x: np.ndarray) -> np.ndarray:
+    """splitmix64 finaliser (Steele, Lea, Flood 2014) on uint64 arrays."""
+    with np.errstate(over="ignore"):
+        z = x + np.uint64(0x9E3779B97F4A7C15)
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return z ^ (z >> np.uint64(31))
+
+
+def accuracy_model_keys(seed: int, jobs, generated, remaining, mae: float) -> np.ndarray:
+    """Stand-in for a trained predictor's outputs (float32): remaining + Laplace(0, mae) noise.
+
+    The noise of job j after g generated tokens is a fixed function of (seed, j, g) (counter-based,
+    so it does not depend on when or how often the job is re-scored): u = uniform (0, 1) from
+    splitmix64, noise = -mae * sign(u - 1/2) * ln(1 - 2 |u - 1/2|). A Laplace(0, b) variable has
+    mean absolute value b."""
+    j = np.asarray(jobs, dtype=np.uint64)
+    g = np.asarray(generated, dtype=np.uint64)
+    with np.errstate(over="ignore"):
+        x = _splitmix64(_splitmix64(np.uint64(seed) ^ (j * np.uint64(0xD1B54A32D192ED03))) ^ g)
+    u = ((x >> np.uint64(11)).astype(np.float64) + 0.5) * 2.0 ** -53
+    d = u - 0.5
+    noise = -mae * np.sign(d) * np.log1p(-2.0 * np.abs(d))
+    return (np.asarray(remaining, dtype=np.float64) + noise).astype(np.float32)
 
 
 def head_is_linear(shape: EncoderShape) -> bool:
