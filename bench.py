@@ -95,7 +95,7 @@ CLASS_KERNELS = {
                                            "paper_2505_09142_amd/csrc/common.h"]),
     "gemm_o": ("gemm_sched_kernel<128, 128, 2, 2, 32, 4, 64, 2, 2>", _GEMM_SRC),
     "layernorm": ("layernorm_kernel<3>", ["paper_2505_09142_amd/csrc/norm.hip", "paper_2505_09142_amd/csrc/common.h"]),
-    "gemm_ffn1": ("gemm_dlds_kernel<256, 256, 2, 4, 32, 2, 1, 64>", _GEMM_SRC),
+    "gemm_ffn1": ("gemm_sched_kernel<256, 256, 2, 4, 32, 1, 64, 1, 2>", _GEMM_SRC),
     "gemm_ffn2": ("gemm_sched_kernel<128, 128, 2, 2, 32, 5, 64, 2, 2>", _GEMM_SRC),
 }
 COPY_KERNEL = "__amd_rocclr_copyBuffer"

@@ -837,9 +837,7 @@ hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, 
 hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uint16_t* w, const float* bias,
                               Residual res, int m, int n, int k, int epi, void* out, hipStream_t st) {
     switch (cfg) {
-        case 0: return launch_tile<128, 128, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
         case 1: return launch_tile<128, 64, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
-        case 14: return launch_dlds<256, 256, 2, 4, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 19: return launch_dlds<128, 128, 2, 2, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 21: return launch_sched<256, 256, 2, 4, 32>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 32: return launch_sched<128, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
@@ -850,27 +848,54 @@ hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uin
 int gemm_config_bn(int cfg) {
     switch (cfg) {
         case 1: return 64;
-        case 14: case 21: return 256;
+        case 21: return 256;
         default: return 128;
     }
 }
 
-// Per-shape choice, from measurements on MI355X over the encoder's GEMM shapes
-// (M = 24K..110K tokens; (N, K) = (3d, d), (d, d), (F, d), (d, F)):
-//   bf16 out, bias (QKV):            8-wave scheduled 256 x 256, staged epilogue
-//   bf16 out, bias + GELU (FFN1):    8-wave 256 x 256 direct-to-LDS
-//   fp32 out, bias + residual:       4-wave 128 x 128 direct-to-LDS; the 8-wave 256 x 256
-//                                    one when K is long and M large (FFN2 at >= 48K tokens)
+// Compute units of the current device (cached per device; the wave-quantisation rule below
+// needs it).
+int device_cus() {
+    static int cus[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cus[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cus[dev] = v;
+    }
+    return cus[dev];
+}
+
+// Per-shape choice, from sweeps on MI355X over the encoder's GEMM shapes (M = 12K..92K
+// tokens; (N, K) = (3d, d), (d, d), (F, d), (d, F)):
+//   bf16 out (QKV; FFN1 with GELU):  8-wave scheduled 256 x 256, staged epilogue
+//   fp32 out + residual (out-proj, FFN2): the same 256 x 256 kernel (one work-group per CU),
+//       unless its last round of tiles is nearly empty: then the 4-wave 128 x 128 scheduled
+//       kernel (two work-groups per CU, four times the tiles) fills the machine better. A
+//       256 x 256 round costs about as much as 1.7 (K = 3072) to 1.9 (K = 768) rounds of the
+//       128 x 128 pairs, hence the rule below.
+// Every configuration accumulates each output element in the same order with the same MFMA
+// instruction and applies the same epilogue arithmetic, so the routing never changes a result.
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
                        int k, int epi, void* out, hipStream_t st) {
     if (m < 1 || n % 64 != 0 || k % kBK != 0 || n < 64 || k < kBK) return hipErrorInvalidValue;
     constexpr int kGroupM = 8;
     const bool n256 = n % 256 == 0, n128 = n % 128 == 0;
+    const bool f32out = epi == ELIS_EPI_BIAS_RES_F32 || kResLnCode(epi);
     int cfg = n128 ? 19 : 1;
-    if (epi == ELIS_EPI_BIAS_BF16 && n256) cfg = 21;
-    else if (epi == ELIS_EPI_BIAS_GELU_BF16 && n256) cfg = 14;
-    else if ((epi == ELIS_EPI_BIAS_RES_F32 || kResLnCode(epi)) && n256 && k >= 2048 && m >= 49152) cfg = 14;
-    else if (kResLnCode(epi) && n128) cfg = 32;
+    if (!f32out && n256) {
+        cfg = 21;
+    } else if (f32out && n128) {
+        cfg = 32;
+        if (n256) {
+            const long long cus = device_cus();
+            const long long t256 = static_cast<long long>((m + 255) / 256) * (n / 256);
+            const long long t128 = static_cast<long long>((m + 127) / 128) * (n / 128);
+            const long long r256 = (t256 + cus - 1) / cus, r128 = (t128 + 2 * cus - 1) / (2 * cus);
+            if (r256 * 100 <= r128 * (k >= 2048 ? 60 : 53)) cfg = 21;
+        }
+    }
     return launch_gemm_config(cfg, cfg == 1 ? 1 : kGroupM, x, w, bias, res, m, n, k, epi, out, st);
 }
 

@@ -310,3 +310,36 @@ def test_linear_large_m_sampled(epi):
         got = bf16_to_f64(host_u16(out[torch.from_numpy(rows).cuda()]))
         ref = oracle.gelu(pre) if epi == E.ELIS_EPI_BIAS_GELU_BF16 else pre
         assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1.2 * acc_tol)
+
+
+def test_linear_routes_agree_bitwise():
+    """Shapes routed to different tile configurations accumulate every output element in the same
+    order with the same instruction and the same epilogue arithmetic: a row (column) computed by
+    one configuration equals the same row (column) computed by another, bit for bit. This is what
+    keeps the predictor's outputs independent of how many tokens are packed with a sequence."""
+    rng = np.random.default_rng(77)
+    cases = [  # (m_a, n_a, m_b, n_b, k, epi): a's output is the top-left corner of b's
+        (23931, 768, 36864, 768, 3072, E.ELIS_EPI_BIAS_RES_F32),   # 128x128 pairs vs 256x256
+        (23931, 768, 40960, 768, 768, E.ELIS_EPI_BIAS_RES_F32),
+        (3000, 384, 3000, 512, 768, E.ELIS_EPI_BIAS_GELU_BF16),     # direct-to-LDS 128x128 vs 256x256
+        (3000, 384, 3000, 512, 768, E.ELIS_EPI_BIAS_BF16),
+    ]
+    for m_a, n_a, m_b, n_b, k, epi in cases:
+        note(f"linear routes m={m_a}/{m_b} n={n_a}/{n_b} k={k} epi={epi}")
+        xb = f32_to_bf16_bits(rng.standard_normal((m_b, k), dtype=np.float32))
+        wb = f32_to_bf16_bits(rng.standard_normal((n_b, k), dtype=np.float32) * 0.05)
+        bias = (rng.standard_normal(n_b) * 0.1).astype(np.float32)
+        f32 = epi == E.ELIS_EPI_BIAS_RES_F32
+        res = rng.standard_normal((m_b, n_b), dtype=np.float32) if f32 else None
+        outs = []
+        for m, n in ((m_a, n_a), (m_b, n_b)):
+            d_x, d_w, d_bias = dev(xb[:m]), dev(wb[:n]), dev(bias[:n])
+            d_res = dev(np.ascontiguousarray(res[:m, :n])) if f32 else None
+            out = torch.empty((m, n), dtype=torch.float32 if f32 else torch.int16, device="cuda")
+            ok(E.elis_linear(d_x.data_ptr(), d_w.data_ptr(), d_bias.data_ptr(), d_res.data_ptr() if f32 else None,
+                             m, n, k, epi, out.data_ptr(), stream()))
+            torch.cuda.synchronize()
+            outs.append(out.cpu().numpy())
+        a, b = outs
+        assert np.array_equal(a.view(np.uint32 if f32 else np.uint16),
+                              np.ascontiguousarray(b[:m_a, :n_a]).view(np.uint32 if f32 else np.uint16))
