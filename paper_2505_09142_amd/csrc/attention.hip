@@ -15,11 +15,15 @@
 // 16-key block in the accumulator layout; those accumulators, rounded to bf16,
 // are directly the lane's slice of the P^T operand of the second product (the
 // 8 k-slots of lane group g are keys {4g..4g+3} and {16+4g..16+4g+3} of a
-// 32-key chunk). The row maximum and row sum of a query are therefore a
-// reduction over the lane's own registers plus two cross-lane shuffles
-// (lanes l, l^16, l^32, l^48 share a query).
+// 32-key chunk). The row maximum of a query is therefore a reduction over the
+// lane's own registers plus two lane-pair exchanges (v_permlane16_swap and
+// v_permlane32_swap: lanes l, l^16, l^32, l^48 share a query). The row sum
+// comes from the matrix cores: one extra 16-row block of O^T whose V^T rows are
+// all ones accumulates sum_k P[q][k] over the same bf16 P that multiplies V, so
+// the output is normalised by exactly the weights it was built from.
 //
-// LDS. K is stored row-major with 16-byte chunks XOR-swizzled by row; V is
+// LDS. K is stored row-major with 16-byte chunks XOR-swizzled by row pairs
+// (the 16 rows one fragment read touches then cover every bank once); V is
 // stored transposed (V^T[d][key], rows padded to 72 keys) so that a lane's
 // 8 keys for one d are two 8-byte reads. Two LDS buffers: the next tile is
 // fetched from HBM into registers while the current one is multiplied, so
@@ -41,9 +45,19 @@ static_assert(kBQ == kAttnRowsPerBlock, "tile table and kernel must agree");
 
 template <int DH>
 __device__ __forceinline__ int kswz(int row) {
-    // chunks per K row: DH/8 (8 for d_head 64, 4 for 32)
+    // chunks per K row: DH/8 (8 for d_head 64, 4 for 32). A 16-row fragment read with 16 bytes
+    // per lane is conflict-free when (bank group of the row start, chunk) is distinct over the
+    // 16 rows: rows start on 2 (d_head 64) or 4 (d_head 32) bank groups.
     constexpr int CPR = DH / 8;
-    return CPR == 8 ? (row & 7) : ((row >> 1) & 3);
+    return CPR == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+}
+
+// Maximum over the lanes l, l^16, l^32, l^48 (the four lanes that hold one query's scores).
+__device__ __forceinline__ float quad_max(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));  // {v of lane l & ~16, v of lane l | 16}
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));  // {l & 31, l | 32}
 }
 
 template <int DH>
@@ -90,8 +104,11 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int j = 0; j < 2; ++j) o[dt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 lsum[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};  // row sums (every register)
     float m_run[2] = {-INFINITY, -INFINITY};
-    float l_run[2] = {0.f, 0.f};
+    bf16x8 ones;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
 
     // Staging of one 64-key tile: K as 16-byte row chunks, V as pairs of rows (2 keys x 8 d).
     constexpr int KCH = kBKV * CPR;                 // K chunks per tile
@@ -208,8 +225,7 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 #pragma unroll
             for (int tt = 1; tt < 4; ++tt)
                 mx = fmaxf(mx, fmaxf(fmaxf(sc[tt][j][0], sc[tt][j][1]), fmaxf(sc[tt][j][2], sc[tt][j][3])));
-            mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+            mx = quad_max(mx);
             const float m_new = fmaxf(m_run[j], mx);
             // alpha < 1 only where this tile raised the running maximum; once the maximum
             // has settled (the common case after the first tiles) the whole wave skips the
@@ -219,18 +235,14 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
             m_run[j] = m_new;
             const float nb = -m_new * scale_log2;
             float p[4][4];
-            float rs = 0.f;
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    p[tt][r] = __builtin_amdgcn_exp2f(fmaf(sc[tt][j][r], scale_log2, nb));
-                    rs += p[tt][r];
-                }
-            l_run[j] = fmaf(l_run[j], alpha, rs);
+                for (int r = 0; r < 4; ++r) p[tt][r] = __builtin_amdgcn_exp2f(fmaf(sc[tt][j][r], scale_log2, nb));
             if (rescale) {
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) o[dt][j] *= alpha;
+                lsum[j] *= alpha;
             }
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
@@ -262,15 +274,16 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                     o[dt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc][j], o[dt][j], 0, 0, 0);
             }
         }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) lsum[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[kc][j], lsum[j], 0, 0, 0);
     }
 
     // Normalise and store: lane holds O[query j*16 + r16][d = dt*16 + 4g .. +3].
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-        float l = l_run[j];
-        l += __shfl_xor(l, 16, kWave);
-        l += __shfl_xor(l, 32, kWave);
-        const float inv = 1.0f / l;
+        const float inv = 1.0f / lsum[j][0];
         const int qi = qw + j * 16 + r16;
         if (qi >= L) continue;
         uint16_t* orow = out + static_cast<size_t>(seq0 + qi) * D + h * DH;
