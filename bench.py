@@ -413,6 +413,110 @@ def isrtf_rounds(max_rounds=None):
     print(json.dumps({"isrtf_rounds": out}), flush=True)
 
 
+ROUNDS100_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b256_x100_rounds.md")
+
+
+def rounds_b256():
+    """The 100-round workload on the device job table: 256 in-flight sequences (prompt +
+    generated-so-far, truncated to 512), each gaining one token per round; every round appends
+    the new tokens, packs all 256 inputs on the device, re-predicts them and selects 128. Latency
+    per round = host wall time from the append to the chosen slots on the host; GPU time per
+    round = HIP events around append + pack + predict + select on the stream."""
+    import numpy as np
+    import torch
+
+    from paper_2505_09142_amd.device import DeviceWeights, Predictor
+    from paper_2505_09142_amd.driver import DeviceRoundDriver
+    from workloads import W_BERT_B256_ROUNDS as w, make_weights
+    from workloads.gen import RoundStream
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    W = make_weights(w.shape, w.weight_seed)
+    pr = Predictor(DeviceWeights(w.shape, W.device, dev), dev)
+    rs = RoundStream(w)
+    n = w.n_seqs
+    base = (rs.prompt + rs.gen0).astype(np.int64)
+    prompts = [st[:int(b)] for st, b in zip(rs.streams, base)]
+    responses = [st[int(b):] for st, b in zip(rs.streams, base)]
+    jobs = list(range(n))
+
+    def run(rounds):
+        drv = DeviceRoundDriver(pr, n, w.shape.max_pos, dev)
+        drv.start(jobs, rs.arrival)
+        gen = np.zeros(n, dtype=np.int64)
+        wall, gpu, toks = [], [], []
+        for r in range(rounds):
+            gen[:] = r
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0 = time.perf_counter()
+            e0.record()
+            drv.sync_tokens(jobs, prompts, responses, gen)
+            drv.predict(jobs)
+            chosen = drv.select(jobs, w.batch_cap)
+            e1.record()
+            wall.append(time.perf_counter() - t0)
+            torch.cuda.synchronize()
+            gpu.append(e0.elapsed_time(e1) * 1e-3)
+            toks.append(int(np.minimum(base + r, w.shape.max_pos).sum()))
+            assert len(chosen) == w.batch_cap
+        st, bits = drv.table.status()
+        if st != 0:
+            raise SystemExit(f"job table status {st} bits {bits}")
+        return np.array(wall), np.array(gpu), np.array(toks)
+
+    run(3)  # warm-up
+    wall, gpu, toks = run(w.rounds)
+    out = {"workload": f"{w.name}: {n} in-flight sequences, BERT-base-shaped predictor, +1 token per round, "
+                       f"select {w.batch_cap}, {w.rounds} rounds on the device job table",
+           "rounds": int(w.rounds), "tokens_round0": int(toks[0]), "tokens_round_last": int(toks[-1]),
+           "p50_ms": float(np.percentile(wall, 50) * 1e3), "p99_ms": float(np.percentile(wall, 99) * 1e3),
+           "gpu_p50_ms": float(np.percentile(gpu, 50) * 1e3), "gpu_mean_ms": float(gpu.mean() * 1e3),
+           "seqs_per_s": float(n * len(gpu) / gpu.sum()), "tokens_per_s": float(toks.sum() / gpu.sum()),
+           "gpu_ms_round0": float(gpu[0] * 1e3), "gpu_ms_round_last": float(gpu[-1] * 1e3)}
+    print(json.dumps({"rounds_b256": out}), flush=True)
+
+
+def summarize_rounds100(js, command):
+    rec = json.loads(open(js).read().strip().splitlines()[-1])["rounds_b256"]
+    lines = ["# 100 scheduling rounds at 256 in-flight sequences (BERT-base-shaped predictor)", "",
+             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             f"{rec['workload']}. Every round appends each sequence's new token to the device job table, packs "
+             "all 256 inputs on the device (first token plus the most recent 511 past 512), re-predicts every one "
+             "and selects 128; one host synchronisation per round (the chosen slots).", "",
+             "| rounds | tokens (round 0 → last) | GPU ms / round (p50, mean) | GPU ms round 0 → last | host wall ms / round (p50, p99) | seqs/s | tokens/s |",
+             "|---:|---|---|---|---|---:|---:|",
+             f"| {rec['rounds']} | {rec['tokens_round0']:,} → {rec['tokens_round_last']:,} | {rec['gpu_p50_ms']:.2f}, "
+             f"{rec['gpu_mean_ms']:.2f} | {rec['gpu_ms_round0']:.2f} → {rec['gpu_ms_round_last']:.2f} | "
+             f"{rec['p50_ms']:.2f}, {rec['p99_ms']:.2f} | {rec['seqs_per_s']:,.0f} | {rec['tokens_per_s']:,.0f} |"]
+    with open(ROUNDS100_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {ROUNDS100_PROFILE}")
+
+
+WORKLOADS_PROFILE = os.path.join(ROOT, "profiles", "workloads_summary.md")
+
+
+def summarize_workloads(paths, command):
+    """One table over bench.py lines of several --workload runs."""
+    lines = ["# Predict + select per workload (one MI355X)", "",
+             "Command (GPU box, repo root as working tree), once per workload:", "", f"    {command}", "",
+             "One step = elis_predict_remaining + elis_isrtf_select on a batch resident in HBM; GEMM and attention "
+             "MFMA utilisation = algorithmic FLOPs / per-class kernel time / 2.5 PFLOP/s (HIP events around each "
+             "launch); the roofline column is bench.py's dominant kernel class.", "",
+             "| workload | sequences | tokens | ms / step (p50) | seqs/s | tokens/s | GEMM MFMA util | attention MFMA util | dominant kernel (frac of peak) |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---|"]
+    for pth in paths:
+        d = json.loads([x for x in open(pth) if x.startswith("{")][-1])
+        c, rf = d["config"], d["roofline"]
+        name = c["workload"].split(":")[0]
+        lines.append(f"| {name} | {c['n_seqs']} | {c['total_tokens']:,} | {d['p50_ms']:.3f} | {d['value']:,.0f} | "
+                     f"{d['tokens_per_s']:,.0f} | {d['mfma_util_gemm']:.3f} | {d['mfma_util_attention']:.3f} | "
+                     f"{rf['kernel']} ({rf['frac']:.3f}) |")
+    with open(WORKLOADS_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {WORKLOADS_PROFILE}")
+
+
 POLICY_PROFILE = os.path.join(ROOT, "profiles", "policy_study.md")
 
 
@@ -560,6 +664,12 @@ def main():
                     help="write the ISRTF round-latency summary")
     ap.add_argument("--isrtf-rounds", action="store_true",
                     help="per-round latency of the ISRTF loop: device job table vs host packing")
+    ap.add_argument("--rounds-b256", action="store_true",
+                    help="the 100-round, 256-sequence workload on the device job table (per-round latency)")
+    ap.add_argument("--summarize-rounds-b256", nargs=2, metavar=("JSON", "COMMAND"),
+                    help="write the 100-round summary")
+    ap.add_argument("--summarize-workloads", nargs="+", metavar="BENCH_JSON",
+                    help="write the per-workload summary from several bench.py lines (last arg: the command)")
     ap.add_argument("--policy-study", action="store_true",
                     help="FCFS / ISRTF / SJF, aging and re-prefill cost on the device job table (Fig. 5/6 analogue)")
     ap.add_argument("--summarize-policy", nargs=2, metavar=("STUDY_JSON", "COMMAND"),
@@ -578,6 +688,15 @@ def main():
         return
     if args.isrtf_rounds:
         isrtf_rounds()
+        return
+    if args.rounds_b256:
+        rounds_b256()
+        return
+    if args.summarize_rounds_b256:
+        summarize_rounds100(*args.summarize_rounds_b256)
+        return
+    if args.summarize_workloads:
+        summarize_workloads(args.summarize_workloads[:-1], args.summarize_workloads[-1])
         return
     if args.policy_study:
         policy_study()
