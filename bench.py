@@ -185,6 +185,45 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, workload, commands):
     print(f"wrote {TRAFFIC_PROFILE}")
 
 
+MFMA_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_mfma_busy.md")
+
+
+def summarize_mfma(csv_path, bench_json, command):
+    """MFMA busy fraction per kernel from one rocprofv3 --pmc pass with SQ_VALU_MFMA_BUSY_CYCLES and
+    SQ_BUSY_CYCLES, next to bench.py's algorithmic utilisation from the same run."""
+    import collections
+    import csv
+    rec = json.loads([x for x in open(bench_json) if x.startswith("{")][-1])
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            n = re.sub(r"\(.*", "", r["Kernel_Name"].replace("elis::(anonymous namespace)::", "").replace("void ", "")).strip()
+            vals[n][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    simds, ses = 1024, 32  # MI355X: 256 CUs x 4 SIMDs; 8 XCDs x 4 shader engines
+    lines = ["# MFMA busy per kernel: bert_base_b64, rocprofv3 PMC counters", "",
+             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "busy = SQ_VALU_MFMA_BUSY_CYCLES / 1024 SIMDs ÷ (SQ_BUSY_CYCLES / 32 shader engines): the fraction of "
+             "the kernel's busy cycles in which an average SIMD's matrix core was working. `algorithmic` = "
+             "bench.py's FLOPs ÷ kernel time ÷ 2.5 PFLOP/s from the same run; the ratio algorithmic / busy is "
+             "(clock under load) ÷ 2.4 GHz when the matrix cores run at their full rate while busy.", "",
+             "| class | kernel | dispatches | MFMA busy | algorithmic | algorithmic / busy |",
+             "|---|---|---:|---:|---:|---:|"]
+    for cls, (kname, _) in CLASS_KERNELS.items():
+        v = vals.get(kname)
+        if not v or not v.get("SQ_VALU_MFMA_BUSY_CYCLES"):
+            continue
+        mb = sum(v["SQ_VALU_MFMA_BUSY_CYCLES"]) / len(v["SQ_VALU_MFMA_BUSY_CYCLES"])
+        bc = sum(v["SQ_BUSY_CYCLES"]) / len(v["SQ_BUSY_CYCLES"])
+        busy = mb / simds / (bc / ses)
+        k = rec["kernels"].get(cls, {})
+        alg = k.get("tflops", 0.0) / PEAK_BF16_TFLOPS if "tflops" in k else None
+        lines.append(f"| {cls} | `{kname}` | {len(v['SQ_BUSY_CYCLES'])} | {busy:.3f} | "
+                     + (f"{alg:.3f} | {alg / busy:.2f} |" if alg is not None and busy > 0 else "- | - |"))
+    with open(MFMA_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {MFMA_PROFILE}")
+
+
 TRACE_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_kernel_trace.md")
 _ROLES = {"seqmap_kernel": "sequence table", "embed_ln_kernel<3>": "embedding + LN",
           "select_rank_kernel": "ISRTF select", "head_hidden_kernel": "head 768->256 + ReLU",
@@ -680,6 +719,8 @@ def main():
                     help="write the large-n select summary")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("STATS_CSV", "BENCH_JSON", "COMMAND"),
                     help="write the kernel-trace summary from a rocprofv3 kernel_stats.csv")
+    ap.add_argument("--summarize-mfma", nargs=3, metavar=("PMC_CSV", "BENCH_JSON", "COMMAND"),
+                    help="write the MFMA-busy summary from a SQ_VALU_MFMA_BUSY_CYCLES / SQ_BUSY_CYCLES pass")
     ap.add_argument("--pmc-command", action="append", default=[],
                     help="with --summarize-pmc: the command of each pass, recorded in the summary")
     args = ap.parse_args()
@@ -712,6 +753,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace[0], args.summarize_trace[2], args.summarize_trace[1])
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma)
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.copy_calibration_mib, args.workload, args.pmc_command)
