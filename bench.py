@@ -67,8 +67,8 @@ def _algorithmic(w, b):
         "layernorm": ("byte", T * (d * (4.0 + 2.0) + 8.0), 2 * L),
         # ids + gathered bf16 word and position rows in; fp32 pre-norm + bf16 rows + stats out
         "embed_ln": ("byte", T * (4.0 + d * (2.0 + 2.0 + 4.0 + 2.0) + 8.0), 1),
-        # pooled rows in + every head weight once
-        "pool_head": ("byte", n * d * 4.0 + 4.0 * _head_params(s), 1),
+        # the hidden rows pooling reads (CLS: one per sequence; mean: every token) + every head weight once
+        "pool_head": ("byte", (n if s.pooling == 0 else T) * d * 4.0 + 4.0 * _head_params(s), 1),
         "seqmap": ("byte", (n + 1) * 4.0 * 4, 1),
         "select": ("byte", n * 12.0 + w.batch_cap * 4.0, 1),
     }
