@@ -181,3 +181,20 @@ def test_device_content_errors_are_flagged():
         assert st == E.ELIS_EDEVICE and bits & bit, (what, st, bits)
     note("valid batch after errors: status clears")
     run(pr, b)
+
+
+def test_checkpoint_loads_into_hbm(tmp_path):
+    """A predictor saved to a checkpoint and loaded back into HBM predicts bit for bit what the
+    in-memory weights predict."""
+    from paper_2505_09142_amd.checkpoint import load_predictor, save_predictor
+    w = W_TINY_HEAD8
+    W, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    note("checkpoint round trip into HBM (tiny shape, 8-layer head)")
+    p1, h1, _ = run(pr, b)
+    path = str(tmp_path / "pred.safetensors")
+    save_predictor(path, w.shape, W.device)
+    cfg, tensors = load_predictor(path)
+    pr2 = Predictor(DeviceWeights(cfg, tensors))
+    p2, h2, _ = run(pr2, b)
+    assert np.array_equal(p1, p2) and np.array_equal(h1, h2)
