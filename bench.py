@@ -9,7 +9,8 @@ weights are in HBM before the timed region starts.
 Prints ONE JSON line. `value` is predicted sequences per second; tokens/s and
 the p50/p99 predict+select latency per round ride along. `roofline` is for the
 kernel class with the largest share of GPU time, timed live over the timed
-region with HIP events on the launch stream (the library's opt-in timing);
+region with HIP events attached to its dispatches on the launch stream (the
+library's opt-in timing, on every 13th launch of the class);
 `cpu_baseline` is the fp64 oracle on a bounded sample of the same batch.
 """
 from __future__ import annotations
@@ -256,7 +257,8 @@ def summarize_trace(stats_csv, command, bench_json):
              "| kernel | class | calls | total µs | avg µs | % of GPU time |", "|---|---|---:|---:|---:|---:|"]
     lines += rows
     lines += ["", f"bench.py's own line in that run: {rec['ms_per_step']:.3f} ms per step, {rec['value']:.0f} seqs/s. "
-              f"Dominant class `{dom}`: {rl['avg_launch_us']:.1f} µs per launch by bench.py's live HIP events vs "
+              f"Dominant class `{dom}`: {rl['avg_launch_us']:.1f} µs per launch by bench.py's live HIP events "
+              f"({rl['launches']} sampled launches, every {rl.get('timing_stride', 1)}th) vs "
               + (f"{prof_us:.1f} µs" if prof_us else "n/a") + " (rocprofv3 average above); "
               f"{rl['per_launch_flop'] / 1e9:.1f} GFLOP per launch -> {rl['achieved']:.0f} {rl['unit']} = "
               f"{100 * rl['frac']:.1f}% of the {rl['peak']:.0f} {rl['unit']} dense bf16 peak."]
@@ -823,8 +825,14 @@ def main():
                          ("tflops" if kind == "flop" else "gbs"): rate}
     dominant = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
 
-    # Timed region: events around the dominant class only, plus per-step events.
+    # Timed region: per-step events, and the dominant class timed on a sample of its launches:
+    # every `stride`-th launch, stride coprime to the launches per step so that the sample rotates
+    # over the layers. A timed dispatch costs a few microseconds of idle GPU around it, which
+    # timing every launch would add to the step time.
+    per_step = round(kernels[dominant]["launches_per_step"])
+    stride = next(s for s in (13, 17, 19, 23) if per_step % s)
     E.elis_timing_reset()
+    E.elis_timing_stride(stride)
     E.elis_timing_enable(1 << E.K[dominant])
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -836,6 +844,7 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     E.elis_timing_enable(0)
+    E.elis_timing_stride(1)
     _, dl, dms = E.elis_timing_read(E.K[dominant])
     elapsed = t1 - t0
     lat = np.array([a.elapsed_time(c) for a, c in evs])
@@ -878,7 +887,7 @@ def main():
         "roofline": {"bound": bound, "kernel": dominant, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": _traffic(dominant),
                      "per_launch_" + ("flop" if kind == "flop" else "bytes"): per_launch,
-                     "avg_launch_us": avg_s * 1e6, "launches": dl},
+                     "avg_launch_us": avg_s * 1e6, "launches": dl, "timing_stride": stride},
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:

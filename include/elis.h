@@ -315,10 +315,14 @@ int elis_layernorm(const float *x, const float *g, const float *b, int32_t rows,
                    float eps, float *out_f32, uint16_t *out_bf16, void *stream);
 
 /* ------------------------------------------------------------------ timing (opt-in)
- * When enabled, the library brackets each kernel launch of the classes below
- * with a pair of HIP events on the launch stream. elis_timing_read
- * synchronises those events and returns, per class, the number of launches
- * and the summed kernel time since the last reset. Process-global state; not
+ * When a class is enabled, each timed launch of it enqueues its kernels with
+ * a start/stop HIP event pair attached to each dispatch (hipExtLaunchKernel),
+ * so the events carry the kernels' own start and end times. With a stride s
+ * (elis_timing_stride, default 1) only every s-th launch of a class since the
+ * last reset is timed; the others run untimed. elis_timing_read synchronises
+ * the pending events and returns, per class, the number of timed launches and
+ * their summed kernel time (a launch that enqueues several kernels counts
+ * once, with the sum of its kernels' times). Process-global state; not
  * thread-safe; meant for benchmarks.
  */
 #define ELIS_K_SEQMAP    0
@@ -335,10 +339,11 @@ int elis_layernorm(const float *x, const float *g, const float *b, int32_t rows,
 #define ELIS_K_COUNT     11
 
 int elis_timing_enable(uint32_t class_mask); /* bit c enables class c; 0 disables */
-int elis_timing_reset(void);
+int elis_timing_stride(int32_t every);       /* every >= 1, else ELIS_EINVAL */
+int elis_timing_reset(void);                 /* also restarts the stride count */
 int elis_timing_read(int32_t kernel_class, int32_t *launches, double *total_ms);
 
-/* ABI version of this header: 2. */
+/* ABI version of this header: 3. */
 int32_t elis_abi_version(void);
 
 #ifdef __cplusplus

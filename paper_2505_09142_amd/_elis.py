@@ -109,6 +109,7 @@ SIGNATURES = {
     "elis_jobs_select_aged": (c_int, [POINTER(elis_job_table), c_void_p, c_void_p, c_float, c_int32, c_int32,
                                       c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "elis_timing_enable": (c_int, [c_uint32]),
+    "elis_timing_stride": (c_int, [c_int32]),
     "elis_timing_reset": (c_int, []),
     "elis_timing_read": (c_int, [c_int32, POINTER(c_int32), POINTER(c_double)]),
 }
@@ -242,6 +243,10 @@ def elis_jobs_select_aged(t: elis_job_table, slots: int, wait: int, aging: float
 
 def elis_timing_enable(class_mask: int) -> int:
     return lib().elis_timing_enable(class_mask)
+
+
+def elis_timing_stride(every: int) -> int:
+    return lib().elis_timing_stride(every)
 
 
 def elis_timing_reset() -> int:

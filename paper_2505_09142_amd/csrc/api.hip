@@ -13,8 +13,11 @@ using namespace elis;
 namespace {
 
 // ------------------------------------------------------------------ timing facility
+// One record per timed kernel launch; `first` marks the first kernel of a class launch
+// (a class launch may enqueue several kernels, e.g. the head's two).
 struct TimedLaunch {
     int cls;
+    bool first;
     hipEvent_t a, b;
 };
 uint32_t g_timing_mask = 0;
@@ -22,6 +25,11 @@ std::vector<TimedLaunch> g_pending;
 std::vector<hipEvent_t> g_free_events;
 double g_ms[ELIS_K_COUNT];
 int32_t g_count[ELIS_K_COUNT];
+uint32_t g_stride = 1;              // time one class launch in every g_stride
+uint64_t g_seen[ELIS_K_COUNT];       // class launches enqueued since the last reset
+int g_timed_cls = -1;  // class being enqueued under timing, else -1
+bool g_timed_first = false;
+bool g_timing_failed = false;
 
 hipEvent_t take_event() {
     if (!g_free_events.empty()) {
@@ -34,20 +42,27 @@ hipEvent_t take_event() {
     return e;
 }
 
-// Runs one launch; when its class is being timed, brackets it with events.
+// Runs one class launch; when its class is being timed, every kernel it enqueues
+// carries its own start/stop events (launch_timing_events below).
 template <class F>
-hipError_t timed(int cls, hipStream_t st, F&& launch) {
+hipError_t timed(int cls, F&& launch) {
     if (!(g_timing_mask & (1u << cls))) return launch();
-    hipEvent_t a = take_event(), b = take_event();
-    if (!a || !b) return hipErrorOutOfMemory;
-    hipError_t e = hipEventRecord(a, st);
-    if (e != hipSuccess) return e;
-    e = launch();
-    if (e != hipSuccess) return e;
-    e = hipEventRecord(b, st);
-    if (e != hipSuccess) return e;
-    g_pending.push_back({cls, a, b});
-    return hipSuccess;
+    if (g_seen[cls]++ % g_stride != 0) return launch();
+    const size_t mark = g_pending.size();
+    g_timed_cls = cls;
+    g_timed_first = true;
+    g_timing_failed = false;
+    const hipError_t e = launch();
+    g_timed_cls = -1;
+    if (e != hipSuccess) {  // drop the records of a class launch that did not complete
+        for (size_t i = mark; i < g_pending.size(); ++i) {
+            g_free_events.push_back(g_pending[i].a);
+            g_free_events.push_back(g_pending[i].b);
+        }
+        g_pending.resize(mark);
+        return e;
+    }
+    return g_timing_failed ? hipErrorOutOfMemory : hipSuccess;
 }
 
 int status_of(hipError_t e) {
@@ -149,9 +164,26 @@ T* at(void* base, size_t off) {
 
 }  // namespace
 
+bool elis::launch_timing_events(hipEvent_t* start, hipEvent_t* stop) {
+    *start = *stop = nullptr;
+    if (g_timed_cls < 0) return false;
+    hipEvent_t a = take_event(), b = take_event();
+    if (!a || !b) {
+        if (a) g_free_events.push_back(a);
+        if (b) g_free_events.push_back(b);
+        g_timing_failed = true;
+        return false;
+    }
+    g_pending.push_back({g_timed_cls, g_timed_first, a, b});
+    g_timed_first = false;
+    *start = a;
+    *stop = b;
+    return true;
+}
+
 extern "C" {
 
-int32_t elis_abi_version(void) { return 2; }
+int32_t elis_abi_version(void) { return 3; }
 
 const char* elis_status_string(int s) {
     switch (s) {
@@ -206,9 +238,9 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
     uint16_t* ffn = L ? at<uint16_t>(workspace, p.ffn) : nullptr;
 
     hipError_t e;
-    e = timed(ELIS_K_SEQMAP, st, [&] { return launch_seqmap(cu_seqlens, n, T, max_seqlen, tab, status, st); });
+    e = timed(ELIS_K_SEQMAP, [&] { return launch_seqmap(cu_seqlens, n, T, max_seqlen, tab, status, st); });
     if (e != hipSuccess) return status_of(e);
-    e = timed(ELIS_K_EMBED_LN, st, [&] {
+    e = timed(ELIS_K_EMBED_LN, [&] {
         const LnOut o = L ? LnOut{nullptr, xb, hb, sb} : LnOut{final32, nullptr, nullptr, nullptr};
         return launch_embed_ln(token_ids, cu_seqlens, n, T, w->word, w->pos, w->type0, w->emb_ln_g, w->emb_ln_b, d,
                                c.vocab, c.max_pos, c.ln_eps, o, status, st);
@@ -220,31 +252,31 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
     for (int l = 0; l < L; ++l) {
         const elis_layer_weights& y = w->layers[l];
         const bool last = (l == L - 1);
-        e = timed(ELIS_K_GEMM_QKV, st, [&] {
+        e = timed(ELIS_K_GEMM_QKV, [&] {
             return launch_gemm(xb, y.w_qkv, y.b_qkv, Residual{}, T, 3 * d, d, ELIS_EPI_BIAS_BF16, qkv, st);
         });
         if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_ATTENTION, st,
+        e = timed(ELIS_K_ATTENTION,
                   [&] { return launch_attention(qkv, tab, n, T, c.n_heads, d / c.n_heads, attn, st); });
         if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_GEMM_O, st, [&] {
+        e = timed(ELIS_K_GEMM_O, [&] {
             return launch_gemm(attn, y.w_o, y.b_o, Residual{hb, sb, prev_g, prev_b}, T, d, d, kEpiResLn, ha, st);
         });
         if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_LAYERNORM, st, [&] {
+        e = timed(ELIS_K_LAYERNORM, [&] {
             return launch_layernorm(ha, y.ln1_g, y.ln1_b, T, d, c.ln_eps, LnOut{nullptr, xb, nullptr, sa}, st);
         });
         if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_GEMM_FFN1, st, [&] {
+        e = timed(ELIS_K_GEMM_FFN1, [&] {
             return launch_gemm(xb, y.w_1, y.b_1, Residual{}, T, F, d, ELIS_EPI_BIAS_GELU_BF16, ffn, st);
         });
         if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_GEMM_FFN2, st, [&] {
+        e = timed(ELIS_K_GEMM_FFN2, [&] {
             return launch_gemm(ffn, y.w_2, y.b_2, Residual{ha, sa, y.ln1_g, y.ln1_b}, T, d, F, kEpiResLnFfn2, hb,
                                st);
         });
         if (e != hipSuccess) return status_of(e);
-        e = timed(ELIS_K_LAYERNORM, st, [&] {
+        e = timed(ELIS_K_LAYERNORM, [&] {
             const LnOut o = last ? LnOut{final32, nullptr, nullptr, nullptr} : LnOut{nullptr, xb, nullptr, sb};
             return launch_layernorm(hb, y.ln2_g, y.ln2_b, T, d, c.ln_eps, o, st);
         });
@@ -252,7 +284,7 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
         prev_g = y.ln2_g;
         prev_b = y.ln2_b;
     }
-    e = timed(ELIS_K_POOL_HEAD, st, [&] {
+    e = timed(ELIS_K_POOL_HEAD, [&] {
         float* hid = c.head_layers >= 2 ? at<float>(workspace, p.head_hid) : nullptr;
         const PoolScratch scr{c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_partial) : nullptr,
                               c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_z) : nullptr, hid,
@@ -282,7 +314,7 @@ int elis_isrtf_select(const float* pred, const int64_t* arrival_seq, int32_t n, 
     if ((batch_cap < n ? batch_cap : n) > select_max_k(n)) return ELIS_EUNSUPPORTED;
     if (ws_bytes < select_workspace_bytes(n)) return ELIS_EWORKSPACE;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e = timed(ELIS_K_SELECT, st, [&] {
+    hipError_t e = timed(ELIS_K_SELECT, [&] {
         return launch_select(pred, arrival_seq, n, batch_cap, out_idx, out_count, workspace, st);
     });
     return status_of(e);
@@ -307,7 +339,7 @@ int elis_jobs_init(const elis_job_table* t, void* stream) {
     int r = check_table(t);
     if (r != ELIS_OK) return r;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    return status_of(timed(ELIS_K_JOBS, st,
+    return status_of(timed(ELIS_K_JOBS,
                            [&] { return launch_jobs_init(jobs_table(t->base, t->max_jobs, t->max_pos), st); }));
 }
 
@@ -318,7 +350,7 @@ int elis_jobs_start(const elis_job_table* t, const int32_t* slots, const int64_t
     if (m < 0 || (m > 0 && (!slots || !arrival_seq))) return ELIS_EINVAL;
     if (m == 0) return ELIS_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    return status_of(timed(ELIS_K_JOBS, st, [&] {
+    return status_of(timed(ELIS_K_JOBS, [&] {
         return launch_jobs_start(jobs_table(t->base, t->max_jobs, t->max_pos), slots, arrival_seq, m, st);
     }));
 }
@@ -331,7 +363,7 @@ int elis_jobs_append(const elis_job_table* t, const int32_t* slots, const int32_
     if (m == 0) return ELIS_OK;
     if (!slots || !tok_offsets || (total_new > 0 && !tokens)) return ELIS_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    return status_of(timed(ELIS_K_JOBS, st, [&] {
+    return status_of(timed(ELIS_K_JOBS, [&] {
         return launch_jobs_append(jobs_table(t->base, t->max_jobs, t->max_pos), slots, tok_offsets, tokens, m,
                                   total_new, st);
     }));
@@ -344,7 +376,7 @@ int elis_jobs_pack(const elis_job_table* t, const int32_t* slots, int32_t n, int
     if (!slots || !out_token_ids || !out_cu_seqlens || n <= 0) return ELIS_EINVAL;
     if (total_tokens < n || max_seqlen < 1 || max_seqlen > t->max_pos) return ELIS_ESHAPE;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    return status_of(timed(ELIS_K_JOBS, st, [&] {
+    return status_of(timed(ELIS_K_JOBS, [&] {
         return launch_jobs_pack(jobs_table(t->base, t->max_jobs, t->max_pos), slots, n, total_tokens, max_seqlen,
                                 out_token_ids, out_cu_seqlens, st);
     }));
@@ -357,7 +389,7 @@ int elis_jobs_store_pred(const elis_job_table* t, const int32_t* slots, const fl
     if (n < 0 || (n > 0 && (!slots || !pred))) return ELIS_EINVAL;
     if (n == 0) return ELIS_OK;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    return status_of(timed(ELIS_K_JOBS, st, [&] {
+    return status_of(timed(ELIS_K_JOBS, [&] {
         return launch_jobs_store_pred(jobs_table(t->base, t->max_jobs, t->max_pos), slots, pred, n, st);
     }));
 }
@@ -381,7 +413,7 @@ int jobs_select_common(const elis_job_table* t, const int32_t* slots, const floa
     if ((batch_cap < a ? batch_cap : a) > select_max_k(a)) return ELIS_EUNSUPPORTED;
     if (ws_bytes < jobs_select_workspace_bytes(a)) return ELIS_EWORKSPACE;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    return status_of(timed(ELIS_K_SELECT, st, [&] {
+    return status_of(timed(ELIS_K_SELECT, [&] {
         return launch_jobs_select(jobs_table(t->base, t->max_jobs, t->max_pos), slots, wait, aging, a, batch_cap,
                                   out_slots, out_count, workspace, st);
     }));
@@ -426,7 +458,7 @@ int elis_linear(const uint16_t* x, const uint16_t* w, const float* bias, const f
                     : epilogue == ELIS_EPI_BIAS_RES_F32 ? ELIS_K_GEMM_FFN2
                                                         : ELIS_K_GEMM_QKV;
     const Residual res{epilogue == ELIS_EPI_BIAS_RES_F32 ? residual : nullptr, nullptr, nullptr, nullptr};
-    return status_of(timed(cls, st, [&] { return launch_gemm(x, w, bias, res, m, n, k, epilogue, out, st); }));
+    return status_of(timed(cls, [&] { return launch_gemm(x, w, bias, res, m, n, k, epilogue, out, st); }));
 }
 
 size_t elis_attention_workspace_bytes(int32_t n_seqs, int32_t total_tokens) {
@@ -453,10 +485,10 @@ int elis_attention(const uint16_t* qkv, const int32_t* cu_seqlens, int32_t n_seq
     tab.len = at<int32_t>(workspace, o);
     o += align_up(sizeof(int32_t) * n_seqs);
     tab.tile_off = at<int32_t>(workspace, o);
-    hipError_t e = timed(ELIS_K_SEQMAP, st,
+    hipError_t e = timed(ELIS_K_SEQMAP,
                          [&] { return launch_seqmap(cu_seqlens, n_seqs, total_tokens, max_seqlen, tab, status, st); });
     if (e != hipSuccess) return status_of(e);
-    return status_of(timed(ELIS_K_ATTENTION, st, [&] {
+    return status_of(timed(ELIS_K_ATTENTION, [&] {
         return launch_attention(qkv, tab, n_seqs, total_tokens, n_heads, d_head, out, st);
     }));
 }
@@ -468,12 +500,18 @@ int elis_layernorm(const float* x, const float* g, const float* b, int32_t rows,
     if (d % 64 || d > 2048) return ELIS_EUNSUPPORTED;
     hipStream_t st = static_cast<hipStream_t>(stream);
     return status_of(
-        timed(ELIS_K_LAYERNORM, st,
+        timed(ELIS_K_LAYERNORM,
               [&] { return launch_layernorm(x, g, b, rows, d, eps, LnOut{out_f32, out_bf16, nullptr, nullptr}, st); }));
 }
 
 int elis_timing_enable(uint32_t class_mask) {
     g_timing_mask = class_mask & ((1u << ELIS_K_COUNT) - 1);
+    return ELIS_OK;
+}
+
+int elis_timing_stride(int32_t every) {
+    if (every < 1) return ELIS_EINVAL;
+    g_stride = static_cast<uint32_t>(every);
     return ELIS_OK;
 }
 
@@ -487,6 +525,7 @@ int elis_timing_reset(void) {
     for (int i = 0; i < ELIS_K_COUNT; ++i) {
         g_ms[i] = 0.0;
         g_count[i] = 0;
+        g_seen[i] = 0;
     }
     return ELIS_OK;
 }
@@ -498,7 +537,7 @@ int elis_timing_read(int32_t kernel_class, int32_t* launches, double* total_ms) 
         float ms = 0.f;
         if (hipEventElapsedTime(&ms, t.a, t.b) != hipSuccess) return ELIS_EHIP;
         g_ms[t.cls] += ms;
-        g_count[t.cls] += 1;
+        g_count[t.cls] += t.first ? 1 : 0;
         g_free_events.push_back(t.a);
         g_free_events.push_back(t.b);
     }

@@ -492,23 +492,23 @@ hipError_t launch_dlds(const uint16_t* x, const uint16_t* w, const float* bias, 
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_BF16, BK>), grid, block, 0, st, x,
+            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_BF16, BK>), grid, block, 0, st, x,
                                w, bias, res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_GELU_BF16, BK>), grid, block, 0,
+            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_GELU_BF16, BK>), grid, block, 0,
                                st, x, w, bias, res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_RES_F32, BK>), grid, block, 0, st,
+            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_RES_F32, BK>), grid, block, 0, st,
                                x, w, bias, res, out, m, n, k, group_m);
             break;
         case kEpiResLn:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLn, BK>), grid, block, 0, st, x, w,
+            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLn, BK>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         case kEpiResLnFfn2:
-            hipLaunchKernelGGL((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLnFfn2, BK>), grid, block, 0, st, x, w,
+            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLnFfn2, BK>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         default:
@@ -777,23 +777,23 @@ hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias,
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16, BK, OCC, S>), grid, block, 0, st, x, w, bias,
+            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16, BK, OCC, S>), grid, block, 0, st, x, w, bias,
                                res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16, BK, OCC, S>), grid, block, 0, st, x, w,
+            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16, BK, OCC, S>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, BK, OCC, S>), grid, block, 0, st, x, w,
+            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, BK, OCC, S>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m);
             break;
         case kEpiResLn:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLn, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLn, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
                                out, m, n, k, group_m);
             break;
         case kEpiResLnFfn2:
-            hipLaunchKernelGGL((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
                                out, m, n, k, group_m);
             break;
         default:
@@ -808,23 +808,23 @@ hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, 
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w,
+            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k);
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x,
+            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x,
                                w, bias, res, out, m, n, k);
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
+            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k);
             break;
         case kEpiResLn:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLn>), grid, block, 0, st, x, w, bias,
+            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLn>), grid, block, 0, st, x, w, bias,
                                res, out, m, n, k);
             break;
         case kEpiResLnFfn2:
-            hipLaunchKernelGGL((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2>), grid, block, 0, st, x, w, bias,
+            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2>), grid, block, 0, st, x, w, bias,
                                res, out, m, n, k);
             break;
         default:

@@ -1,6 +1,10 @@
 // Host-side launchers of the libelis kernels (each defined in its own .hip file).
 #pragma once
 
+#include <hip/hip_ext.h>
+
+#include <tuple>
+
 #include "common.h"
 
 namespace elis {
@@ -105,5 +109,31 @@ size_t jobs_select_workspace_bytes(int max_active);
 // wait: null, or fp32 [a] seconds waited, aging the keys by `aging` tokens per second.
 hipError_t launch_jobs_select(JobTable t, const int32_t* slots, const float* wait, float aging, int a, int k,
                               int32_t* out_slots, int32_t* out_count, void* workspace, hipStream_t st);
+
+// ------------------------------------------------------------------ launching
+// Timing hook of the opt-in per-class timing (api.hip): while a timed class is
+// being enqueued it hands out one start/stop event pair per kernel launch;
+// otherwise it returns false and leaves both null.
+bool launch_timing_events(hipEvent_t* start, hipEvent_t* stop);
+
+// Every kernel of the library is enqueued through launch_kernel. When the hook
+// hands out events they travel with the dispatch packet (hipExtLaunchKernel)
+// and take its own start and end timestamps, so timing a class puts no marker
+// packets, and no extra gaps, between the kernels of a forward pass.
+template <typename... P, typename... A>
+inline hipError_t launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t lds, hipStream_t st,
+                                A... a) {
+    static_assert(sizeof...(P) == sizeof...(A), "kernel argument count");
+    std::tuple<P...> args{static_cast<P>(a)...};
+    hipEvent_t start = nullptr, stop = nullptr;
+    launch_timing_events(&start, &stop);
+    return std::apply(
+        [&](auto&... v) {
+            void* ptrs[] = {static_cast<void*>(&v)...};
+            return hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, lds, st, start,
+                                      stop, 0);
+        },
+        args);
+}
 
 }  // namespace elis

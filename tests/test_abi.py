@@ -40,7 +40,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert E.elis_abi_version() == 2
+    assert E.elis_abi_version() == 3
     for s in (0, -1, -2, -3, -4, -5, -6):
         assert E.elis_status_string(s).startswith("ELIS_")
     assert E.elis_status_string(123) == "unknown status"
@@ -188,6 +188,10 @@ def test_timing_api_host_only(lib):
     st, n, ms = E.elis_timing_read(0)
     assert st == 0 and n == 0 and ms == 0.0
     assert E.elis_timing_read(99)[0] == E.ELIS_EINVAL
+    assert E.elis_timing_stride(0) == E.ELIS_EINVAL
+    assert E.elis_timing_stride(-3) == E.ELIS_EINVAL
+    assert E.elis_timing_stride(13) == 0
+    assert E.elis_timing_stride(1) == 0
 
 
 def test_job_table_rejects_invalid_arguments(lib):

@@ -198,3 +198,67 @@ def test_checkpoint_loads_into_hbm(tmp_path):
     pr2 = Predictor(DeviceWeights(cfg, tensors))
     p2, h2, _ = run(pr2, b)
     assert np.array_equal(p1, p2) and np.array_equal(h1, h2)
+
+
+@pytest.mark.parametrize("w", [W_TINY, W_TINY_HEAD8], ids=lambda w: w.name)
+def test_timing_counts_class_launches_and_keeps_results(w):
+    """The opt-in per-class timing: one count per class launch (the head of mean pooling enqueues
+    several kernels and still counts once), positive times, and bitwise the same predictions and
+    selection as an untimed pass."""
+    note(f"timing hook {w.name}")
+    _, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    ids, cu, arr = upload_batch(b)
+    p0, _ = pr.predict(ids, cu, b.max_seqlen)
+    i0, c0 = pr.select(p0, arr, w.batch_cap)
+    torch.cuda.synchronize()
+    E.elis_timing_reset()
+    E.elis_timing_enable((1 << len(E.KERNEL_CLASSES)) - 1)
+    try:
+        for _ in range(2):
+            p1, _ = pr.predict(ids, cu, b.max_seqlen)
+            i1, c1 = pr.select(p1, arr, w.batch_cap)
+        torch.cuda.synchronize()
+    finally:
+        E.elis_timing_enable(0)
+    L = w.shape.n_layers
+    want = {"seqmap": 1, "embed_ln": 1, "gemm_qkv": L, "attention": L, "gemm_o": L, "layernorm": 2 * L,
+            "gemm_ffn1": L, "gemm_ffn2": L, "pool_head": 1, "select": 1}
+    for name in E.KERNEL_CLASSES:
+        st, nl, ms = E.elis_timing_read(E.K[name])
+        assert st == E.ELIS_OK
+        assert nl == 2 * want.get(name, 0), name
+        assert (ms > 0) == (nl > 0), name
+    E.elis_timing_reset()
+    assert E.elis_timing_read(E.K["gemm_qkv"])[1] == 0
+    assert torch.equal(p0, p1)
+    assert int(c0.item()) == int(c1.item())
+    assert torch.equal(i0[:int(c0.item())], i1[:int(c1.item())])
+
+
+def test_timing_stride_samples_class_launches():
+    """With a stride s the timing covers launch 0, s, 2s, ... of each class since the last reset,
+    counted across forward passes (so a stride coprime to the layer count rotates over the layers)."""
+    w = W_TINY
+    note(f"timing stride {w.name}")
+    _, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    ids, cu, arr = upload_batch(b)
+    L, passes, stride = w.shape.n_layers, 5, 3
+    E.elis_timing_reset()
+    assert E.elis_timing_stride(stride) == E.ELIS_OK
+    E.elis_timing_enable((1 << E.K["gemm_ffn2"]) | (1 << E.K["layernorm"]))
+    try:
+        for _ in range(passes):
+            pr.predict(ids, cu, b.max_seqlen)
+        torch.cuda.synchronize()
+    finally:
+        E.elis_timing_enable(0)
+        E.elis_timing_stride(1)
+    for name, per_pass in (("gemm_ffn2", L), ("layernorm", 2 * L)):
+        st, nl, ms = E.elis_timing_read(E.K[name])
+        assert st == E.ELIS_OK
+        assert nl == -(-passes * per_pass // stride), name
+        assert ms > 0
+    assert E.elis_timing_read(E.K["gemm_qkv"])[1] == 0
+    E.elis_timing_reset()
