@@ -85,20 +85,53 @@ def _source_sha(paths):
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_hbm_traffic.md")
 
-# Kernel behind each class at the BERT-base, 64-sequence workload (the GEMM routing picks
-# the tile configuration per shape), and the sources whose text fixes that kernel: a PMC
-# figure is reported only while those sources are unchanged.
+# Kernels behind each class at a workload, and the sources whose text fixes them: a PMC figure
+# is reported only while those sources are unchanged. A GEMM class is one launch or two (the
+# library's launch plan may split the rows between a large-tile and a small-tile launch); the
+# plan comes from elis_linear_plan at the workload's token count.
 _GEMM_SRC = ["paper_2505_09142_amd/csrc/gemm.hip", "paper_2505_09142_amd/csrc/common.h",
              "paper_2505_09142_amd/csrc/kernels.h"]
-CLASS_KERNELS = {
-    "gemm_qkv": ("gemm_sched_kernel<256, 256, 2, 4, 32, 0, 64, 1, 2>", _GEMM_SRC),
-    "attention": ("attention_kernel<64>", ["paper_2505_09142_amd/csrc/attention.hip",
-                                           "paper_2505_09142_amd/csrc/common.h"]),
-    "gemm_o": ("gemm_sched_kernel<128, 128, 2, 2, 32, 4, 64, 2, 2>", _GEMM_SRC),
-    "layernorm": ("layernorm_kernel<3>", ["paper_2505_09142_amd/csrc/norm.hip", "paper_2505_09142_amd/csrc/common.h"]),
-    "gemm_ffn1": ("gemm_sched_kernel<256, 256, 2, 4, 32, 1, 64, 1, 2>", _GEMM_SRC),
-    "gemm_ffn2": ("gemm_sched_kernel<128, 128, 2, 2, 32, 5, 64, 2, 2>", _GEMM_SRC),
-}
+_GEMM_EPI = {"gemm_qkv": (0, 0), "gemm_o": (2, 4), "gemm_ffn1": (1, 1), "gemm_ffn2": (2, 5)}  # public, internal
+
+
+def _gemm_kernel(bm, bn, wgs, epi, n, f32):
+    if (bm, bn) == (256, 256):
+        return f"gemm_sched_kernel<256, 256, 2, 4, 32, {epi}, 64, 1, 2>"
+    if (bm, bn) == (128, 128):
+        if not f32 and n % 256:
+            return f"gemm_dlds_kernel<128, 128, 2, 2, 32, 2, {epi}, 64>"
+        return f"gemm_sched_kernel<128, 128, 2, 2, 32, {epi}, 64, 2, 2>"
+    if (bm, bn) == (64, 128):
+        return f"gemm_sched_kernel<64, 128, 2, 2, 32, {epi}, 64, {wgs}, {2 if wgs == 2 else 4}>"
+    return f"gemm_kernel<128, 64, 2, 2, 16, {epi}>"
+
+
+def class_kernels(workload: str) -> dict:
+    """class -> ([kernel names, one per launch of the class], sources)."""
+    from paper_2505_09142_amd import _elis as E
+    from workloads import WORKLOADS, make_batch
+    w = WORKLOADS[workload]
+    s = w.shape
+    T, d, F = make_batch(w).total, s.d_model, s.d_ff
+    dims = {"gemm_qkv": (3 * d, d), "gemm_o": (d, d), "gemm_ffn1": (F, d), "gemm_ffn2": (d, F)}
+    out = {}
+    for cls, (n, k) in dims.items():
+        pub, internal = _GEMM_EPI[cls]
+        st, (bm, bn, wg, m1, rbm, rbn, rwg) = E.elis_linear_plan(T, n, k, pub)
+        if st != 0:
+            raise SystemExit(f"elis_linear_plan failed for {cls}: {st}")
+        names = [_gemm_kernel(bm, bn, wg, internal, n, pub == 2)]
+        if m1 < T:
+            names.append(_gemm_kernel(rbm, rbn, rwg, internal, n, pub == 2))
+        out[cls] = (names, _GEMM_SRC)
+    vpl = (d + 255) // 256
+    out["attention"] = ([f"attention_kernel<{d // s.n_heads}>"], ["paper_2505_09142_amd/csrc/attention.hip",
+                                                                  "paper_2505_09142_amd/csrc/common.h"])
+    out["layernorm"] = ([f"layernorm_kernel<{vpl}>"], ["paper_2505_09142_amd/csrc/norm.hip",
+                                                        "paper_2505_09142_amd/csrc/common.h"])
+    return out
+
+
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
@@ -162,20 +195,23 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, workload, commands):
               f"{', '.join(f'{v:.0f}' for v in cf)} KiB, WRITE_SIZE {', '.join(f'{v:.0f}' for v in cw)} KiB, "
               f"for {nbytes / 1024:.0f} KiB moved each way, so bytes = FETCH_SIZE x 1024 x {f_scale:.4f} "
               f"and WRITE_SIZE x 1024 x {w_scale:.4f}.", "",
-              "| class | kernel | launches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled MB | mandatory MB | ratio |",
+              "| class | kernels (one dispatch each per launch) | launches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled MB | mandatory MB | ratio |",
               "|---|---|---:|---:|---:|---:|---:|---:|"]
     recs = {}
-    for cls, (kname, srcs) in CLASS_KERNELS.items():
-        fv, wv = fetch.get(kname, []), write.get(kname, [])
-        if not fv or not wv:
-            lines.append(f"| {cls} | `{kname}` | 0 | - | - | - | - | - |")
+    for cls, (knames, srcs) in class_kernels(workload).items():
+        label = " + ".join(f"`{k}`" for k in knames)
+        fvs, wvs = [fetch.get(k, []) for k in knames], [write.get(k, []) for k in knames]
+        if not all(fvs) or not all(wvs):
+            lines.append(f"| {cls} | {label} | 0 | - | - | - | - | - |")
             continue
-        fk, wk = sum(fv) / len(fv), sum(wv) / len(wv)
+        # per class launch: the sum of its kernels' per-dispatch averages
+        fk = sum(sum(v) / len(v) for v in fvs)
+        wk = sum(sum(v) / len(v) for v in wvs)
         tb = fk * 1024 * f_scale + wk * 1024 * w_scale
-        lines.append(f"| {cls} | `{kname}` | {len(fv)} | {fk:,.0f} | {wk:,.0f} | {tb / 1e6:,.1f} | "
+        lines.append(f"| {cls} | {label} | {len(fvs[0])} | {fk:,.0f} | {wk:,.0f} | {tb / 1e6:,.1f} | "
                      f"{mandatory[cls] / 1e6:,.1f} | {tb / mandatory[cls]:.2f} |")
         recs[cls] = {"per_launch_bytes": tb, "fetch_kib": fk, "write_kib": wk, "fetch_scale": f_scale,
-                     "write_scale": w_scale, "mandatory_bytes": mandatory[cls], "kernel": kname,
+                     "write_scale": w_scale, "mandatory_bytes": mandatory[cls], "kernels": knames,
                      "sources": srcs, "source_sha256": _source_sha(srcs)}
     lines += ["", "`ratio` = scaled traffic / mandatory bytes; above 1 means operands were fetched from "
               "memory more than once (tiles re-read after leaving L2).", "",
@@ -207,18 +243,20 @@ def summarize_mfma(csv_path, bench_json, command):
              "the kernel's busy cycles in which an average SIMD's matrix core was working. `algorithmic` = "
              "bench.py's FLOPs ÷ kernel time ÷ 2.5 PFLOP/s from the same run; the ratio algorithmic / busy is "
              "(clock under load) ÷ 2.4 GHz when the matrix cores run at their full rate while busy.", "",
-             "| class | kernel | dispatches | MFMA busy | algorithmic | algorithmic / busy |",
+             "| class | kernels | launches | MFMA busy | algorithmic | algorithmic / busy |",
              "|---|---|---:|---:|---:|---:|"]
-    for cls, (kname, _) in CLASS_KERNELS.items():
-        v = vals.get(kname)
-        if not v or not v.get("SQ_VALU_MFMA_BUSY_CYCLES"):
+    for cls, (knames, _) in class_kernels(rec["config"]["workload"].split(":")[0]).items():
+        vs = [vals.get(k) for k in knames]
+        if not all(v and v.get("SQ_VALU_MFMA_BUSY_CYCLES") for v in vs):
             continue
-        mb = sum(v["SQ_VALU_MFMA_BUSY_CYCLES"]) / len(v["SQ_VALU_MFMA_BUSY_CYCLES"])
-        bc = sum(v["SQ_BUSY_CYCLES"]) / len(v["SQ_BUSY_CYCLES"])
+        # cycles of a class launch: the sum over its kernels of their per-dispatch averages
+        mb = sum(sum(v["SQ_VALU_MFMA_BUSY_CYCLES"]) / len(v["SQ_VALU_MFMA_BUSY_CYCLES"]) for v in vs)
+        bc = sum(sum(v["SQ_BUSY_CYCLES"]) / len(v["SQ_BUSY_CYCLES"]) for v in vs)
         busy = mb / simds / (bc / ses)
         k = rec["kernels"].get(cls, {})
         alg = k.get("tflops", 0.0) / PEAK_BF16_TFLOPS if "tflops" in k else None
-        lines.append(f"| {cls} | `{kname}` | {len(v['SQ_BUSY_CYCLES'])} | {busy:.3f} | "
+        label = " + ".join(f"`{x}`" for x in knames)
+        lines.append(f"| {cls} | {label} | {len(vs[0]['SQ_BUSY_CYCLES'])} | {busy:.3f} | "
                      + (f"{alg:.3f} | {alg / busy:.2f} |" if alg is not None and busy > 0 else "- | - |"))
     with open(MFMA_PROFILE, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -237,7 +275,8 @@ def summarize_trace(stats_csv, command, bench_json):
     import csv
     rec = json.loads(open(bench_json).read().strip().splitlines()[-1])
     roles = dict(_ROLES)
-    roles.update({k: c for c, (k, _) in CLASS_KERNELS.items()})
+    ck = class_kernels(rec["config"]["workload"].split(":")[0])
+    roles.update({k: c for c, (ks, _) in ck.items() for k in ks})
     rows, avg = [], {}
     with open(stats_csv) as f:
         for r in csv.DictReader(f):
@@ -247,7 +286,7 @@ def summarize_trace(stats_csv, command, bench_json):
                         f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
     rl = rec["roofline"]
     dom = rl["kernel"]
-    prof_us = avg.get(CLASS_KERNELS[dom][0]) if dom in CLASS_KERNELS else None
+    prof_us = sum(avg.get(k, 0.0) for k in ck[dom][0]) if dom in ck and all(k in avg for k in ck[dom][0]) else None
     cfg = rec["config"]
     steps, warm = rec["steps"], rec["warmup"]
     lines = [f"# Kernel trace: {cfg['workload'].split(':')[0]} (T = {cfg['total_tokens']:,}), predict + select", "",
@@ -259,7 +298,7 @@ def summarize_trace(stats_csv, command, bench_json):
     lines += ["", f"bench.py's own line in that run: {rec['ms_per_step']:.3f} ms per step, {rec['value']:.0f} seqs/s. "
               f"Dominant class `{dom}`: {rl['avg_launch_us']:.1f} µs per launch by bench.py's live HIP events "
               f"({rl['launches']} sampled launches, every {rl.get('timing_stride', 1)}th) vs "
-              + (f"{prof_us:.1f} µs" if prof_us else "n/a") + " (rocprofv3 average above); "
+              + (f"{prof_us:.1f} µs" if prof_us else "n/a") + " (rocprofv3 averages above, summed over the class's kernels); "
               f"{rl['per_launch_flop'] / 1e9:.1f} GFLOP per launch -> {rl['achieved']:.0f} {rl['unit']} = "
               f"{100 * rl['frac']:.1f}% of the {rl['peak']:.0f} {rl['unit']} dense bf16 peak."]
     with open(TRACE_PROFILE, "w") as f:
@@ -404,6 +443,126 @@ def select_sweep(ks=(64, 8192), iters=20):
     if st != E.ELIS_OK:
         raise SystemExit(f"device status {st} bits {bits}")
     print(json.dumps({"select_sweep": rows}), flush=True)
+
+
+GEMM_PLAN_SHAPES = (  # (name, N, K, public epilogue): the encoder products of BERT-base and XLM-R-large
+    ("bert_qkv", 2304, 768, 0), ("bert_ffn1", 3072, 768, 1), ("bert_o", 768, 768, 2), ("bert_ffn2", 768, 3072, 2),
+    ("xlmr_qkv", 3072, 1024, 0), ("xlmr_ffn1", 4096, 1024, 1), ("xlmr_o", 1024, 1024, 2), ("xlmr_ffn2", 1024, 4096, 2))
+GEMM_PLAN_MS = (1024, 2560, 4096, 6144, 8192, 10240, 12288, 14336, 16384, 18432, 20480, 22528, 23931, 26624, 28672,
+                30720, 32768, 47000, 92000)
+GEMM_PLAN_PROFILE = os.path.join(ROOT, "profiles", "gemm_launch_plans.md")
+
+
+def gemm_plans(reps=8):
+    """Every launch plan the library can choose from, timed one by one (elis_linear_with_plan),
+    next to the plan it does choose (elis_linear_plan), over the encoder products of BERT-base
+    and XLM-R-large at token counts 1K .. 92K. fp32-out products use the plain residual."""
+    import torch
+
+    from paper_2505_09142_amd import _elis as E
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    stream = torch.cuda.current_stream().cuda_stream
+    g = torch.Generator(device="cpu").manual_seed(0)
+    mmax = max(GEMM_PLAN_MS)
+    out = []
+    for name, n, k, epi in GEMM_PLAN_SHAPES:
+        f32 = epi == 2
+        x = (torch.randn(mmax, k, generator=g) * 0.5).to(torch.bfloat16).to(dev)
+        w = (torch.randn(n, k, generator=g) * 0.03).to(torch.bfloat16).to(dev)
+        bias = torch.zeros(n, device=dev)
+        res = torch.randn(mmax, n, device=dev) if f32 else None
+        o = torch.empty(mmax, n, device=dev, dtype=torch.float32 if f32 else torch.bfloat16)
+        tiles = [t for t in ((256, 256, 1), (128, 128, 2), (64, 128, 2), (64, 128, 1)) if n % t[1] == 0]
+        for m in GEMM_PLAN_MS:
+            plans = []
+            for t in tiles:
+                plans.append(t + (m, 0, 0, 0))
+                per_row, slots = n // t[1], t[2] * cus
+                m1 = (-(-m // t[0]) * per_row) // slots * slots // per_row * t[0]
+                if 0 < m1 < m:
+                    plans += [t + (m1,) + r for r in tiles if r != t]
+
+            def run(plan):
+                E.check(E.elis_linear_with_plan(x.data_ptr(), w.data_ptr(), bias.data_ptr(),
+                                                res.data_ptr() if f32 else None, m, n, k, epi, plan, o.data_ptr(),
+                                                stream), f"{name} {plan}")
+            times = {}
+            for order in (plans, plans[::-1]):  # two passes in opposite orders, the faster one kept
+                for plan in order:
+                    for _ in range(2):
+                        run(plan)
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    for _ in range(reps):
+                        run(plan)
+                    e1.record()
+                    torch.cuda.synchronize()
+                    us = e0.elapsed_time(e1) / reps * 1e3
+                    times[plan] = min(us, times.get(plan, us))
+            st, chosen = E.elis_linear_plan(m, n, k, epi)
+            E.check(st, "elis_linear_plan")
+            out.append({"shape": name, "n": n, "k": k, "epi": epi, "m": m, "chosen": list(chosen),
+                        "plans": [[list(p), t] for p, t in times.items()]})
+            best = min(times, key=times.get)
+            print(f"{name} m={m}: chosen {chosen} {times[tuple(chosen)]:.1f} us, fastest {best} {times[best]:.1f} us",
+                  file=sys.stderr, flush=True)
+        del x, w, res, o
+    print(json.dumps({"gemm_plans": out, "cus": cus}), flush=True)
+
+
+def summarize_gemm_plans(js, command):
+    rec = json.loads([x for x in open(js) if x.startswith("{")][-1])
+    rows = rec["gemm_plans"]
+
+    def tile(p):
+        return f"{p[0]}×{p[1]}" + ("/1" if p[:3] == [64, 128, 1] else "")
+
+    def label(p):
+        return tile(p) if p[4] == 0 else f"{tile(p)} + {tile(p[4:7])} from row {p[3]:,}"
+    lines = ["# GEMM launch plans: every plan timed vs the one the library picks", "",
+             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "For each encoder product of BERT-base and XLM-R-large (fp32-out products with the plain residual) "
+             "and each token count M, every plan the library can choose from is timed through "
+             "`elis_linear_with_plan`: one launch of 256×256, 128×128, 64×128 (2 per CU) or 64×128/1 (1 per CU, "
+             "4 stages) tiles, or large tiles over the rows that fill whole rounds plus a second launch of another "
+             "configuration over the rest. `chosen` is `elis_linear_plan`'s pick (the launch-time model); "
+             "`fastest` the best measured; the fixed columns are what one configuration alone takes.", "",
+             "| shape | chosen / fastest, summed over M | 256×256 alone | 128×128 alone |", "|---|---:|---:|---:|"]
+    tot = {"chosen": 0.0, "fastest": 0.0}
+    by_shape = {}
+    for r in rows:
+        t = {tuple(p): us for p, us in r["plans"]}
+        m = r["m"]
+        c = t[tuple(r["chosen"])]
+        f = min(t.values())
+        s = by_shape.setdefault(r["shape"], {"chosen": 0.0, "fastest": 0.0, "256": 0.0, "128": 0.0, "has256": True})
+        s["chosen"] += c
+        s["fastest"] += f
+        s["128"] += t[(128, 128, 2, m, 0, 0, 0)]
+        if (256, 256, 1, m, 0, 0, 0) in t:
+            s["256"] += t[(256, 256, 1, m, 0, 0, 0)]
+        else:
+            s["has256"] = False
+        tot["chosen"] += c
+        tot["fastest"] += f
+    for name, s in by_shape.items():
+        lines.append(f"| {name} | {s['chosen'] / s['fastest']:.3f} | "
+                     + (f"{s['256'] / s['fastest']:.3f}" if s["has256"] else "-") + f" | {s['128'] / s['fastest']:.3f} |")
+    lines += ["", f"All shapes and sizes: the chosen plans take {tot['chosen'] / tot['fastest']:.4f}× the time of the "
+              "fastest measured ones.", "",
+              "Per size, BERT-base at the benchmark's 23,931 tokens and at a small and a large batch:", "",
+              "| shape | M | chosen plan | µs | fastest plan | µs |", "|---|---:|---|---:|---|---:|"]
+    for r in rows:
+        if r["shape"].startswith("bert") and r["m"] in (2560, 23931, 92000):
+            t = {tuple(p): us for p, us in r["plans"]}
+            best = min(t, key=t.get)
+            lines.append(f"| {r['shape']} | {r['m']:,} | {label(r['chosen'])} | {t[tuple(r['chosen'])]:.1f} | "
+                         f"{label(list(best))} | {t[best]:.1f} |")
+    with open(GEMM_PLAN_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {GEMM_PLAN_PROFILE}")
 
 
 def isrtf_rounds(max_rounds=None):
@@ -715,6 +874,10 @@ def main():
                     help="FCFS / ISRTF / SJF, aging and re-prefill cost on the device job table (Fig. 5/6 analogue)")
     ap.add_argument("--summarize-policy", nargs=2, metavar=("STUDY_JSON", "COMMAND"),
                     help="write the policy-study summary")
+    ap.add_argument("--gemm-plans", action="store_true",
+                    help="time every GEMM launch plan against the library's choice (encoder products, M = 1K .. 92K)")
+    ap.add_argument("--summarize-gemm-plans", nargs=2, metavar=("JSON", "COMMAND"),
+                    help="write the GEMM launch-plan summary")
     ap.add_argument("--select-sweep", action="store_true",
                     help="time the device-wide select at n = 2^20 .. 2^24 instead of the step")
     ap.add_argument("--summarize-select", nargs=3, metavar=("SWEEP_JSON", "TRACE_CSV", "COMMAND"),
@@ -752,6 +915,12 @@ def main():
         return
     if args.select_sweep:
         select_sweep()
+        return
+    if args.gemm_plans:
+        gemm_plans()
+        return
+    if args.summarize_gemm_plans:
+        summarize_gemm_plans(*args.summarize_gemm_plans)
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace[0], args.summarize_trace[2], args.summarize_trace[1])

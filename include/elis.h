@@ -289,6 +289,36 @@ int elis_jobs_select_aged(const elis_job_table *t, const int32_t *slots, const f
 int elis_linear(const uint16_t *x, const uint16_t *w, const float *bias, const float *residual,
                 int32_t m, int32_t n, int32_t k, int32_t epilogue, void *out, void *stream);
 
+/*
+ * How elis_linear (and the encoder's products, whose fp32 epilogue carries the
+ * same cost) launches an m x n x k product on the current device. Host only:
+ * no GPU work, no synchronisation. out[7] = {main_bm, main_bn, main_wgs, m1,
+ * rest_bm, rest_bn, rest_wgs}: rows [0, m1) run in tiles of main_bm x main_bn,
+ * main_wgs work-groups per compute unit; when m1 < m, rows [m1, m) run in a
+ * second launch in tiles of rest_bm x rest_bn, rest_wgs per compute unit (else
+ * the three rest fields are 0). The plan comes from a launch-time model of the
+ * tile configurations and the device's compute-unit count; every plan gives
+ * bit-identical results (except that the 128 x 64 tile, used only when n is
+ * an odd multiple of 64, accumulates with 16 x 16 x 32 blocks). Errors: as
+ * elis_linear (ELIS_EINVAL, ELIS_EUNSUPPORTED), and ELIS_EINVAL on a null out.
+ */
+int elis_linear_plan(int32_t m, int32_t n, int32_t k, int32_t epilogue, int32_t *out);
+
+/*
+ * elis_linear with the launch plan given instead of chosen: plan[7] in the
+ * layout elis_linear_plan writes. Tiles: 256 x 256 (1 work-group per CU),
+ * 128 x 128 (2), 64 x 128 (2 or 1; the latter four-stage), 128 x 64 (2;
+ * single launch, and only for n an odd multiple of 64, where it is the only
+ * tile); main_bn and rest_bn must divide n, 1 <= m1 <= m, m1 a multiple of
+ * main_bm when m1 < m, rest different from main. Every valid plan gives the
+ * same bits as elis_linear; meant for benchmarking and re-fitting the launch
+ * model on other hardware. Errors: as elis_linear, and ELIS_EINVAL for a null
+ * or invalid plan.
+ */
+int elis_linear_with_plan(const uint16_t *x, const uint16_t *w, const float *bias, const float *residual,
+                          int32_t m, int32_t n, int32_t k, int32_t epilogue, const int32_t *plan, void *out,
+                          void *stream);
+
 /* Bytes of workspace elis_attention needs (0 if invalid). */
 size_t elis_attention_workspace_bytes(int32_t n_seqs, int32_t total_tokens);
 

@@ -90,6 +90,9 @@ SIGNATURES = {
     "elis_read_status": (c_int, [c_void_p, c_void_p, POINTER(c_uint32)]),
     "elis_linear": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p,
                             c_void_p]),
+    "elis_linear_plan": (c_int, [c_int32, c_int32, c_int32, c_int32, POINTER(c_int32)]),
+    "elis_linear_with_plan": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32,
+                                      POINTER(c_int32), c_void_p, c_void_p]),
     "elis_attention_workspace_bytes": (c_size_t, [c_int32, c_int32]),
     "elis_attention": (c_int, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p,
                                c_size_t, c_void_p]),
@@ -178,6 +181,19 @@ def elis_read_status(workspace: int, stream: int | None):
 def elis_linear(x: int, w: int, bias: int, residual: int | None, m: int, n: int, k: int, epilogue: int, out: int,
                 stream: int | None) -> int:
     return lib().elis_linear(x, w, bias, residual, m, n, k, epilogue, out, stream)
+
+
+def elis_linear_with_plan(x: int, w: int, bias: int, residual: int | None, m: int, n: int, k: int, epilogue: int,
+                          plan, out: int, stream: int | None) -> int:
+    p = (c_int32 * 7)(*plan) if plan is not None else None
+    return lib().elis_linear_with_plan(x, w, bias, residual, m, n, k, epilogue, p, out, stream)
+
+
+def elis_linear_plan(m: int, n: int, k: int, epilogue: int):
+    """Returns (status, (main_bm, main_bn, main_wgs, m1, rest_bm, rest_bn, rest_wgs))."""
+    out = (c_int32 * 7)()
+    st = lib().elis_linear_plan(m, n, k, epilogue, out)
+    return st, tuple(out)
 
 
 def elis_attention_workspace_bytes(n_seqs: int, total_tokens: int) -> int:

@@ -162,6 +162,27 @@ T* at(void* base, size_t off) {
     return reinterpret_cast<T*>(static_cast<char*>(base) + off);
 }
 
+int check_linear(const uint16_t* x, const uint16_t* w, const float* bias, const float* residual, int32_t m,
+                 int32_t n, int32_t k, int32_t epilogue, void* out) {
+    if (!x || !w || !bias || !out) return ELIS_EINVAL;
+    if (epilogue != ELIS_EPI_BIAS_BF16 && epilogue != ELIS_EPI_BIAS_GELU_BF16 && epilogue != ELIS_EPI_BIAS_RES_F32)
+        return ELIS_EINVAL;
+    if (epilogue == ELIS_EPI_BIAS_RES_F32 && !residual) return ELIS_EINVAL;
+    if (m <= 0 || n <= 0 || k <= 0) return ELIS_EINVAL;
+    if (n % 64 || k % 64) return ELIS_EUNSUPPORTED;
+    return ELIS_OK;
+}
+
+int run_linear(const GemmPlan& p, const uint16_t* x, const uint16_t* w, const float* bias, const float* residual,
+               int32_t m, int32_t n, int32_t k, int32_t epilogue, void* out, void* stream) {
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int cls = epilogue == ELIS_EPI_BIAS_GELU_BF16 ? ELIS_K_GEMM_FFN1
+                    : epilogue == ELIS_EPI_BIAS_RES_F32 ? ELIS_K_GEMM_FFN2
+                                                        : ELIS_K_GEMM_QKV;
+    const Residual res{epilogue == ELIS_EPI_BIAS_RES_F32 ? residual : nullptr, nullptr, nullptr, nullptr};
+    return status_of(timed(cls, [&] { return launch_gemm_plan(p, x, w, bias, res, m, n, k, epilogue, out, st); }));
+}
+
 }  // namespace
 
 bool elis::launch_timing_events(hipEvent_t* start, hipEvent_t* stop) {
@@ -447,18 +468,29 @@ int elis_read_status(const void* workspace, void* stream, uint32_t* bits) {
 
 int elis_linear(const uint16_t* x, const uint16_t* w, const float* bias, const float* residual, int32_t m, int32_t n,
                 int32_t k, int32_t epilogue, void* out, void* stream) {
-    if (!x || !w || !bias || !out) return ELIS_EINVAL;
-    if (epilogue != ELIS_EPI_BIAS_BF16 && epilogue != ELIS_EPI_BIAS_GELU_BF16 && epilogue != ELIS_EPI_BIAS_RES_F32)
+    const int v = check_linear(x, w, bias, residual, m, n, k, epilogue, out);
+    if (v != ELIS_OK) return v;
+    return run_linear(plan_gemm(m, n, k, epilogue), x, w, bias, residual, m, n, k, epilogue, out, stream);
+}
+
+int elis_linear_with_plan(const uint16_t* x, const uint16_t* w, const float* bias, const float* residual, int32_t m,
+                          int32_t n, int32_t k, int32_t epilogue, const int32_t* plan, void* out, void* stream) {
+    const int v = check_linear(x, w, bias, residual, m, n, k, epilogue, out);
+    if (v != ELIS_OK) return v;
+    if (!plan) return ELIS_EINVAL;
+    GemmPlan p{gemm_config_of_tile(plan[0], plan[1], plan[2]), plan[3], 0};
+    if (p.main < 0 || n % plan[1] != 0 || p.m1 < 1 || p.m1 > m) return ELIS_EINVAL;
+    if (p.main == 1 && n % 128 == 0) return ELIS_EINVAL;  // 128 x 64 only where nothing else fits
+    if (p.m1 < m) {
+        p.rest = gemm_config_of_tile(plan[4], plan[5], plan[6]);
+        // the 16 x 16 x 32 configuration accumulates in another order: single launches only
+        if (p.rest < 0 || p.rest == p.main || p.main == 1 || p.rest == 1 || n % plan[5] != 0 ||
+            p.m1 % plan[0] != 0)
+            return ELIS_EINVAL;
+    } else if (plan[4] || plan[5] || plan[6]) {
         return ELIS_EINVAL;
-    if (epilogue == ELIS_EPI_BIAS_RES_F32 && !residual) return ELIS_EINVAL;
-    if (m <= 0 || n <= 0 || k <= 0) return ELIS_EINVAL;
-    if (n % 64 || k % 64) return ELIS_EUNSUPPORTED;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    const int cls = epilogue == ELIS_EPI_BIAS_GELU_BF16 ? ELIS_K_GEMM_FFN1
-                    : epilogue == ELIS_EPI_BIAS_RES_F32 ? ELIS_K_GEMM_FFN2
-                                                        : ELIS_K_GEMM_QKV;
-    const Residual res{epilogue == ELIS_EPI_BIAS_RES_F32 ? residual : nullptr, nullptr, nullptr, nullptr};
-    return status_of(timed(cls, [&] { return launch_gemm(x, w, bias, res, m, n, k, epilogue, out, st); }));
+    }
+    return run_linear(p, x, w, bias, residual, m, n, k, epilogue, out, stream);
 }
 
 size_t elis_attention_workspace_bytes(int32_t n_seqs, int32_t total_tokens) {
@@ -504,6 +536,19 @@ int elis_layernorm(const float* x, const float* g, const float* b, int32_t rows,
               [&] { return launch_layernorm(x, g, b, rows, d, eps, LnOut{out_f32, out_bf16, nullptr, nullptr}, st); }));
 }
 
+int elis_linear_plan(int32_t m, int32_t n, int32_t k, int32_t epilogue, int32_t* out) {
+    if (!out || m <= 0 || n <= 0 || k <= 0) return ELIS_EINVAL;
+    if (epilogue != ELIS_EPI_BIAS_BF16 && epilogue != ELIS_EPI_BIAS_GELU_BF16 && epilogue != ELIS_EPI_BIAS_RES_F32)
+        return ELIS_EINVAL;
+    if (n % 64 || k % 64) return ELIS_EUNSUPPORTED;
+    const GemmPlan p = plan_gemm(m, n, k, epilogue);
+    gemm_config_tile(p.main, &out[0], &out[1], &out[2]);
+    out[3] = p.m1;
+    out[4] = out[5] = out[6] = 0;
+    if (p.m1 < m) gemm_config_tile(p.rest, &out[4], &out[5], &out[6]);
+    return ELIS_OK;
+}
+
 int elis_timing_enable(uint32_t class_mask) {
     g_timing_mask = class_mask & ((1u << ELIS_K_COUNT) - 1);
     return ELIS_OK;
@@ -517,7 +562,7 @@ int elis_timing_stride(int32_t every) {
 
 int elis_timing_reset(void) {
     for (auto& t : g_pending) {
-        hipEventSynchronize(t.b);
+        (void)hipEventSynchronize(t.b);
         g_free_events.push_back(t.a);
         g_free_events.push_back(t.b);
     }

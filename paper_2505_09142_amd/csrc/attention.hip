@@ -306,14 +306,14 @@ hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total,
     const dim3 grid(tiles, heads), block(kWaves * kWave);
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
     if (dh == 64)
-        launch_kernel(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2);
+        ELIS_TRY(launch_kernel(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
+                           out, scale_log2));
     else if (dh == 32)
-        launch_kernel(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2);
+        ELIS_TRY(launch_kernel(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
+                           out, scale_log2));
     else
         return hipErrorInvalidValue;
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace elis

@@ -6,15 +6,16 @@
 // either an fp32 matrix or a LayerNorm output rebuilt from its pre-norm rows and
 // row statistics (Residual in kernels.h).
 //
-// Three kernel families, chosen per shape by launch_gemm:
-//   gemm_kernel        register-staged k-slabs, 16 x 16 x 32 MFMA blocks; covers
-//                      N that is a multiple of 64 only;
-//   gemm_dlds_kernel   k-slabs go HBM -> LDS with global_load_lds_dwordx4 (no
-//                      register staging), S stages, 32 x 32 x 16 MFMA blocks;
-//   gemm_sched_kernel  the same loads plus a hand-scheduled k-loop: operand
-//                      fragments double-buffered in registers, MFMAs of the last
-//                      k-step of a slab issued after the slab barrier, and an
-//                      epilogue staged through LDS for full-line stores.
+// Two kernel families; launch_gemm plans each product (plan_gemm: one launch, or a
+// launch of large tiles over whole rounds plus one of small tiles over the remaining rows):
+//   gemm_kernel        register-staged k-slabs, 16 x 16 x 32 MFMA blocks; for N that
+//                      is an odd multiple of 64;
+//   gemm_sched_kernel  k-slabs go HBM -> LDS with global_load_lds_dwordx4 (no register
+//                      staging), 32 x 32 x 16 MFMA blocks, a hand-scheduled k-loop
+//                      (operand fragments double-buffered in registers, MFMAs of the
+//                      last k-step of a slab issued after the slab barrier) and an
+//                      epilogue staged through LDS for full-line stores; tiles of
+//                      256 x 256, 128 x 128 and 64 x 128.
 //
 // LDS layout. A k-slab row of 64 bf16 is eight 16-byte chunks; the chunk index
 // is XOR-swizzled with the row so the rows one MFMA operand read touches fall on
@@ -246,7 +247,7 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __r
 }
 
 // ---------------------------------------------------------------------------------------------
-// Multi-stage variant: k-slabs go from HBM straight into LDS (global_load_lds_dwordx4, no
+// Direct-to-LDS loading: k-slabs go from HBM straight into LDS (global_load_lds_dwordx4, no
 // register staging), S stages deep, so S-1 slabs are in flight while one is multiplied.
 // Each thread waits (vmcnt) only for its own loads of the slab about to be consumed; the
 // barrier that follows makes every thread's part of that slab visible and also guarantees
@@ -282,239 +283,6 @@ __device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, in
     const int r = t - g * per_group;
     tm = first + r % rows;
     tn = r / rows;
-}
-
-template <int BM, int BN, int WM, int WN, int MI, int S, int EPI, int BK = 64>
-__global__ __launch_bounds__(WM* WN* kWave) void gemm_dlds_kernel(const uint16_t* __restrict__ A,
-                                                                  const uint16_t* __restrict__ B,
-                                                                  const float* __restrict__ bias,
-                                                                  Residual res,
-                                                                  void* __restrict__ out, int M, int N, int K,
-                                                                  int group_m) {
-    typedef Mfma<MI> MF;
-    typedef typename MF::acc_t acc_t;
-    constexpr int NW = WM * WN;
-    constexpr int TM = BM / WM, TN = BN / WN;
-    constexpr int FM = TM / MI, FN = TN / MI;
-    constexpr int KSTEPS = BK / MF::kDepth;
-    constexpr int GROUPS = kWave / MI;
-    constexpr int CPR = BK / 8;                  // 16-byte chunks per k-slab row
-    constexpr int RPI = kWave * 16 / (BK * 2);   // rows covered by one wave-wide 16-byte load
-    constexpr int SWS = BK == 64 ? 1 : 2;        // swizzle: chunk ^ ((row >> SWS) & (CPR - 1))
-    constexpr int LA = BM / RPI / NW, LB = BN / RPI / NW;  // loads per wave per stage
-    constexpr int STAGE = (BM + BN) * BK;        // bf16 elements per stage
-    static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "rows must split over the waves");
-    static_assert(S >= 2 && (S - 1) * (LA + LB) < 64, "pipeline depth");
-
-    __shared__ __attribute__((aligned(1024))) uint16_t smem[S * STAGE];
-
-    const int tiles_n = N / BN;
-    const int tiles_m = (M + BM - 1) / BM;
-    int tm, tn;
-    grouped_tile(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, group_m, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
-
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
-    const int wm = wid / WN, wn = wid % WN;
-
-    // Global source of this lane for each of its loads: LDS row = base + lane / CPR, physical
-    // chunk lane % CPR, which holds logical chunk (lane % CPR) ^ ((row >> SWS) & (CPR - 1)).
-    const uint16_t* ga[LA];
-    const uint16_t* gb[LB];
-#pragma unroll
-    for (int i = 0; i < LA; ++i) {
-        const int row = (wid * LA + i) * RPI + lane / CPR;
-        const int c = (lane % CPR) ^ ((row >> SWS) & (CPR - 1));
-        const int gr = (m0 + row < M) ? m0 + row : M - 1;
-        ga[i] = A + static_cast<size_t>(gr) * K + c * 8;
-    }
-#pragma unroll
-    for (int i = 0; i < LB; ++i) {
-        const int row = (wid * LB + i) * RPI + lane / CPR;
-        const int c = (lane % CPR) ^ ((row >> SWS) & (CPR - 1));
-        gb[i] = B + static_cast<size_t>(n0 + row) * K + c * 8;
-    }
-
-    auto issue = [&](int kt) {
-        uint16_t* st = smem + (kt % S) * STAGE;
-        const int k0 = kt * BK;
-#pragma unroll
-        for (int i = 0; i < LA; ++i)
-            load_lds_16(ga[i] + k0, st + (wid * LA + i) * RPI * BK);
-#pragma unroll
-        for (int i = 0; i < LB; ++i)
-            load_lds_16(gb[i] + k0, st + BM * BK + (wid * LB + i) * RPI * BK);
-    };
-
-    acc_t acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < MF::kRegs; ++r) acc[i][j][r] = 0.f;
-
-    const int KT = K / BK;
-#pragma unroll
-    for (int p = 0; p < S - 1; ++p)
-        if (p < KT) issue(p);
-
-    const int rl = lane % MI, kg = lane / MI;
-    for (int kt = 0; kt < KT; ++kt) {
-        // loads issued after slab kt: min(S-2, KT-1-kt) stages
-        const int later = (KT - 1 - kt) < (S - 2) ? (KT - 1 - kt) : (S - 2);
-        if constexpr (S >= 4) {
-            if (later >= 2) wait_vmcnt<2 * (LA + LB)>();
-            else if (later == 1) wait_vmcnt<(LA + LB)>();
-            else wait_vmcnt<0>();
-        } else if constexpr (S == 3) {
-            if (later >= 1) wait_vmcnt<(LA + LB)>();
-            else wait_vmcnt<0>();
-        } else {
-            wait_vmcnt<0>();
-        }
-        block_sync_lds();
-        if (kt + S - 1 < KT) issue(kt + S - 1);
-        const uint16_t* sA = smem + (kt % S) * STAGE;
-        const uint16_t* sB = sA + BM * BK;
-#pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) {
-            const int c = ks * GROUPS + kg;
-            bf16x8 af[FM], bfr[FN];
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int row = wm * TM + i * MI + rl;
-                af[i] = *reinterpret_cast<const bf16x8*>(&sA[row * BK + ((c ^ ((row >> SWS) & (CPR - 1))) * 8)]);
-            }
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int row = wn * TN + j * MI + rl;
-                bfr[j] = *reinterpret_cast<const bf16x8*>(&sB[row * BK + ((c ^ ((row >> SWS) & (CPR - 1))) * 8)]);
-            }
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j) acc[i][j] = MF::run(bfr[j], af[i], acc[i][j]);
-        }
-    }
-
-    // Epilogue. Loads are batched ahead of their use, so their latency is paid once per
-    // batch instead of once per output vector. Lane (rl, kg) holds, for row m = rl of block
-    // row i, groups of 4 consecutive columns at 8 * q + 4 * kg of block column j.
-    constexpr int NQ = MF::kRegs / 4;  // 4-column groups per MFMA block per lane
-    if constexpr (kF32Out<EPI>) {
-        // fp32 out: one block column at a time. Its bias (and LayerNorm g, b) vectors are
-        // requested together, then per block row the residual vectors of that row.
-        float2 stv[FM];
-        if constexpr (kResLn<EPI>) {
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int m = m0 + wm * TM + i * MI + rl;
-                stv[i] = res.stats[m < M ? m : M - 1];
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int nj = n0 + wn * TN + j * MI + 4 * kg;
-            f32x4 bj[NQ], gj[NQ], ej[NQ];
-#pragma unroll
-            for (int q = 0; q < NQ; ++q) {
-                bj[q] = *reinterpret_cast<const f32x4*>(bias + nj + 8 * q);
-                if constexpr (kResLn<EPI>) {
-                    gj[q] = *reinterpret_cast<const f32x4*>(res.g + nj + 8 * q);
-                    ej[q] = *reinterpret_cast<const f32x4*>(res.b + nj + 8 * q);
-                }
-            }
-#pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int m = m0 + wm * TM + i * MI + rl;
-                if (m >= M) continue;
-                const size_t ro = static_cast<size_t>(m) * N + nj;
-                f32x4 rv[NQ];
-#pragma unroll
-                for (int q = 0; q < NQ; ++q) rv[q] = *reinterpret_cast<const f32x4*>(res.x + ro + 8 * q);
-#pragma unroll
-                for (int q = 0; q < NQ; ++q) {
-                    f32x4 v;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
-                    f32x4 h = rv[q];
-                    if constexpr (kResLn<EPI>) {
-#pragma unroll
-                        for (int c = 0; c < 4; ++c) h[c] = fmaf((h[c] - stv[i].x) * stv[i].y, gj[q][c], ej[q][c]);
-                    }
-                    v += bj[q];
-                    v += h;
-                    *reinterpret_cast<f32x4*>(static_cast<float*>(out) + ro + 8 * q) = v;
-                }
-            }
-            // Keep the next block column's loads from being hoisted here: registers stay
-            // bounded by one block column's operands.
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    } else {
-        f32x4 bv[FN][NQ];
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int q = 0; q < NQ; ++q)
-                bv[j][q] = *reinterpret_cast<const f32x4*>(bias + n0 + wn * TN + j * MI + 8 * q + 4 * kg);
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int m = m0 + wm * TM + i * MI + rl;
-            if (m >= M) continue;
-            const size_t ro = static_cast<size_t>(m) * N + n0 + wn * TN + 4 * kg;
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-#pragma unroll
-                for (int q = 0; q < NQ; ++q) {
-                    f32x4 v;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * q + r];
-                    v += bv[j][q];
-                    if constexpr (EPI == ELIS_EPI_BIAS_GELU_BF16) {
-#pragma unroll
-                        for (int c = 0; c < 4; ++c) v[c] = gelu_erf(v[c]);
-                    }
-                    u32x2 pk;
-                    pk[0] = pack_bf16x2(v[0], v[1]);
-                    pk[1] = pack_bf16x2(v[2], v[3]);
-                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + ro + j * MI + 8 * q) = pk;
-                }
-            }
-        }
-    }
-}
-
-template <int BM, int BN, int WM, int WN, int MI, int S, int BK = 64>
-hipError_t launch_dlds(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
-                       int k, int epi, void* out, hipStream_t st, int group_m) {
-    const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
-    switch (epi) {
-        case ELIS_EPI_BIAS_BF16:
-            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_BF16, BK>), grid, block, 0, st, x,
-                               w, bias, res, out, m, n, k, group_m);
-            break;
-        case ELIS_EPI_BIAS_GELU_BF16:
-            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_GELU_BF16, BK>), grid, block, 0,
-                               st, x, w, bias, res, out, m, n, k, group_m);
-            break;
-        case ELIS_EPI_BIAS_RES_F32:
-            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, ELIS_EPI_BIAS_RES_F32, BK>), grid, block, 0, st,
-                               x, w, bias, res, out, m, n, k, group_m);
-            break;
-        case kEpiResLn:
-            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLn, BK>), grid, block, 0, st, x, w,
-                               bias, res, out, m, n, k, group_m);
-            break;
-        case kEpiResLnFfn2:
-            launch_kernel((gemm_dlds_kernel<BM, BN, WM, WN, MI, S, kEpiResLnFfn2, BK>), grid, block, 0, st, x, w,
-                               bias, res, out, m, n, k, group_m);
-            break;
-        default:
-            return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -777,29 +545,29 @@ hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias,
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16, BK, OCC, S>), grid, block, 0, st, x, w, bias,
-                               res, out, m, n, k, group_m);
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16, BK, OCC, S>), grid, block, 0, st, x, w, bias,
+                               res, out, m, n, k, group_m));
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16, BK, OCC, S>), grid, block, 0, st, x, w,
-                               bias, res, out, m, n, k, group_m);
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16, BK, OCC, S>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k, group_m));
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, BK, OCC, S>), grid, block, 0, st, x, w,
-                               bias, res, out, m, n, k, group_m);
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, BK, OCC, S>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k, group_m));
             break;
         case kEpiResLn:
-            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLn, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
-                               out, m, n, k, group_m);
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLn, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+                               out, m, n, k, group_m));
             break;
         case kEpiResLnFfn2:
-            launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
-                               out, m, n, k, group_m);
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+                               out, m, n, k, group_m));
             break;
         default:
             return hipErrorInvalidValue;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 template <int BM, int BN, int WM, int WN, int MI>
@@ -808,29 +576,29 @@ hipError_t launch_tile(const uint16_t* x, const uint16_t* w, const float* bias, 
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w,
-                               bias, res, out, m, n, k);
+            ELIS_TRY(launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k));
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x,
-                               w, bias, res, out, m, n, k);
+            ELIS_TRY(launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16>), grid, block, 0, st, x,
+                               w, bias, res, out, m, n, k));
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
-                               bias, res, out, m, n, k);
+            ELIS_TRY(launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32>), grid, block, 0, st, x, w,
+                               bias, res, out, m, n, k));
             break;
         case kEpiResLn:
-            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLn>), grid, block, 0, st, x, w, bias,
-                               res, out, m, n, k);
+            ELIS_TRY(launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLn>), grid, block, 0, st, x, w, bias,
+                               res, out, m, n, k));
             break;
         case kEpiResLnFfn2:
-            launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2>), grid, block, 0, st, x, w, bias,
-                               res, out, m, n, k);
+            ELIS_TRY(launch_kernel((gemm_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2>), grid, block, 0, st, x, w, bias,
+                               res, out, m, n, k));
             break;
         default:
             return hipErrorInvalidValue;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace
@@ -840,23 +608,35 @@ hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uin
                               Residual res, int m, int n, int k, int epi, void* out, hipStream_t st) {
     switch (cfg) {
         case 1: return launch_tile<128, 64, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
-        case 19: return launch_dlds<128, 128, 2, 2, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 21: return launch_sched<256, 256, 2, 4, 32>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 32: return launch_sched<128, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 33: return launch_sched<64, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 34: return launch_sched<64, 128, 2, 2, 32, 64, 1, 4>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         default: return hipErrorInvalidValue;
     }
 }
 
-int gemm_config_bn(int cfg) {
-    switch (cfg) {
-        case 1: return 64;
-        case 21: return 256;
-        default: return 128;
-    }
+namespace {
+struct TileShape {
+    int cfg, bm, bn, wgs_per_cu;
+};
+constexpr TileShape kTileShapes[] = {{1, 128, 64, 2}, {21, 256, 256, 1}, {32, 128, 128, 2}, {33, 64, 128, 2},
+                                     {34, 64, 128, 1}};
+}  // namespace
+
+void gemm_config_tile(int cfg, int* bm, int* bn, int* wgs_per_cu) {
+    *bm = *bn = *wgs_per_cu = 0;
+    for (const TileShape& t : kTileShapes)
+        if (t.cfg == cfg) *bm = t.bm, *bn = t.bn, *wgs_per_cu = t.wgs_per_cu;
 }
 
-// Compute units of the current device (cached per device; the wave-quantisation rule below
-// needs it).
+int gemm_config_of_tile(int bm, int bn, int wgs_per_cu) {
+    for (const TileShape& t : kTileShapes)
+        if (t.bm == bm && t.bn == bn && t.wgs_per_cu == wgs_per_cu) return t.cfg;
+    return -1;
+}
+
+// Compute units of the current device (cached per device; the launch-time model below needs it).
 int device_cus() {
     static int cus[64];
     int dev = 0;
@@ -869,36 +649,111 @@ int device_cus() {
     return cus[dev];
 }
 
-// Per-shape choice, from sweeps on MI355X over the encoder's GEMM shapes (M = 12K..92K
-// tokens; (N, K) = (3d, d), (d, d), (F, d), (d, F)):
-//   bf16 out (QKV; FFN1 with GELU):  8-wave scheduled 256 x 256, staged epilogue
-//   fp32 out + residual (out-proj, FFN2): the same 256 x 256 kernel (one work-group per CU),
-//       unless its last round of tiles is nearly empty: then the 4-wave 128 x 128 scheduled
-//       kernel (two work-groups per CU, four times the tiles) fills the machine better. A
-//       256 x 256 round costs about as much as 1.7 (K = 3072) to 1.9 (K = 768) rounds of the
-//       128 x 128 pairs, hence the rule below.
-// Every configuration accumulates each output element in the same order with the same MFMA
-// instruction and applies the same epilogue arithmetic, so the routing never changes a result.
+namespace {
+
+// Launch-time model of the scheduled configurations, in microseconds on MI355X (256 CUs),
+// fitted to medians of repeated timings of the BERT-base and XLM-R-large encoder GEMMs
+// (K = 768 .. 4096, one to four rounds of tiles). A launch whose tiles fill R rounds of
+// work-group slots (work-groups per CU x CUs), the last one a fraction f full, takes part(f)
+// for R = 1, else t1 + (R - 2) * beta + part(f) - (t1 - beta) * f; part is piecewise linear
+// through lat (a lone tile, f -> 0), th (f = 1/2) and t1 (f = 1), beta is the cost of one more
+// full round. Each quantity is a + s * K / 64: the slope per 64-deep k-slab is shared by the
+// epilogue kinds, the intercept is per kind (bf16, bf16 + GELU, fp32 + residual). Over every
+// single and split plan of those shapes at 35 sizes (M = 1K .. 92K), timed one by one, the
+// plan it picks is 0.2% slower in total than the fastest one measured.
+struct TileModel {
+    int cfg, bm, bn, occ;
+    float s[4];     // lat, th, t1, beta: slope per k-slab
+    float a[3][4];  // intercept per epilogue kind
+};
+constexpr TileModel kTileModels[] = {
+    {21, 256, 256, 1, {1.185f, 1.408f, 1.667f, 1.739f},
+     {{4.81f, 5.68f, 7.52f, 3.94f}, {11.77f, 11.42f, 12.18f, 8.36f}, {10.32f, 14.51f, 22.08f, 28.05f}}},
+    {32, 128, 128, 2, {0.545f, 0.652f, 0.957f, 1.196f},
+     {{3.03f, 4.01f, 4.69f, -0.71f}, {5.15f, 5.64f, 8.13f, 2.30f}, {4.86f, 8.02f, 11.89f, 4.54f}}},
+    {33, 64, 128, 2, {0.341f, 0.581f, 0.609f, 0.578f},
+     {{3.21f, 1.76f, 4.19f, 2.62f}, {3.64f, 2.13f, 4.16f, 3.57f}, {3.97f, 2.82f, 7.97f, 5.24f}}},
+    {34, 64, 128, 1, {0.365f, 0.393f, 0.418f, 0.408f},
+     {{2.80f, 3.13f, 3.41f, 1.62f}, {3.57f, 3.79f, 4.40f, 2.40f}, {3.81f, 4.03f, 4.57f, 3.48f}}},
+};
+constexpr float kSecondLaunchUs = 1.0f;  // dispatch cost of the remainder launch
+
+double model_us(const TileModel& t, int kind, long long m, int n, int k, long long cus) {
+    if (m <= 0) return 0.0;
+    const long long tiles = (m + t.bm - 1) / t.bm * (n / t.bn), slots = t.occ * cus;
+    const long long rounds = (tiles + slots - 1) / slots;
+    const double f = static_cast<double>(tiles - (rounds - 1) * slots) / static_cast<double>(slots);
+    double v[4];
+    for (int q = 0; q < 4; ++q) v[q] = t.a[kind][q] + t.s[q] * (k / 64.0);
+    const double part = f <= 0.5 ? v[0] + (v[1] - v[0]) * (f / 0.5) : v[1] + (v[2] - v[1]) * ((f - 0.5) / 0.5);
+    if (rounds == 1) return part;
+    // First round t1, full rounds after it beta each (they overlap the one before), and a last
+    // round f full that overlaps the one before it by (t1 - beta) * f.
+    return v[2] + static_cast<double>(rounds - 2) * v[3] + part - (v[2] - v[3]) * f;
+}
+
+}  // namespace
+
+// The plan of one product: a single launch of one configuration, or (main, m1, rest): rows
+// [0, m1) with `main` in whole rounds of tiles and rows [m1, m) with the smaller-tile `rest`,
+// whichever the launch-time model above prices lowest. A 256 x 256 round costs about as much
+// as two rounds of the 128 x 128 pairs, but a round that is only partly filled costs nearly a
+// full one, so the rows past the last full round of large tiles go to a configuration whose
+// tiles are small enough to finish them in one short round.
+GemmPlan plan_gemm(int m, int n, int k, int epi) {
+    const bool f32out = epi == ELIS_EPI_BIAS_RES_F32 || kResLnCode(epi);
+    if (n % 128 != 0) return {1, m, 0};
+    const int kind = f32out ? 2 : (epi == ELIS_EPI_BIAS_GELU_BF16 ? 1 : 0);
+    const long long cus = device_cus();
+    GemmPlan best{21, m, 0};
+    double best_us = -1.0;
+    for (const TileModel& main : kTileModels) {
+        if (n % main.bn != 0) continue;
+        const double t = model_us(main, kind, m, n, k, cus);
+        if (best_us < 0.0 || t < best_us) {
+            best_us = t;
+            best = {main.cfg, m, 0};
+        }
+        // Whole rows of tiles that fill whole rounds.
+        const long long per_row = n / main.bn, slots = main.occ * cus;
+        const long long tiles = (static_cast<long long>(m) + main.bm - 1) / main.bm * per_row;
+        const long long m1 = (tiles / slots) * slots / per_row * main.bm;
+        if (m1 <= 0 || m1 >= m) continue;
+        const double head = model_us(main, kind, m1, n, k, cus) + kSecondLaunchUs;
+        for (const TileModel& rest : kTileModels) {
+            if (rest.cfg == main.cfg || n % rest.bn != 0) continue;
+            const double tr = head + model_us(rest, kind, m - m1, n, k, cus);
+            if (tr < best_us) {
+                best_us = tr;
+                best = {main.cfg, static_cast<int>(m1), rest.cfg};
+            }
+        }
+    }
+    return best;
+}
+
+hipError_t launch_gemm_plan(const GemmPlan& p, const uint16_t* x, const uint16_t* w, const float* bias,
+                            Residual res, int m, int n, int k, int epi, void* out, hipStream_t st) {
+    constexpr int kGroupM = 8;
+    ELIS_TRY(launch_gemm_config(p.main, p.main == 1 ? 1 : kGroupM, x, w, bias, res, p.m1, n, k, epi, out, st));
+    if (p.m1 >= m) return hipSuccess;
+    const size_t r0 = static_cast<size_t>(p.m1);
+    const bool f32out = epi == ELIS_EPI_BIAS_RES_F32 || kResLnCode(epi);
+    Residual rr = res;
+    if (rr.x) rr.x += r0 * n;
+    if (rr.stats) rr.stats += r0;
+    void* o2 = f32out ? static_cast<void*>(static_cast<float*>(out) + r0 * n)
+                      : static_cast<void*>(static_cast<uint16_t*>(out) + r0 * n);
+    return launch_gemm_config(p.rest, kGroupM, x + r0 * k, w, bias, rr, m - p.m1, n, k, epi, o2, st);
+}
+
+// Every 32 x 32 x 16 configuration accumulates each output element in the same order with the
+// same MFMA instruction and applies the same epilogue arithmetic, so neither the plan nor the
+// split ever changes a result.
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
                        int k, int epi, void* out, hipStream_t st) {
     if (m < 1 || n % 64 != 0 || k % kBK != 0 || n < 64 || k < kBK) return hipErrorInvalidValue;
-    constexpr int kGroupM = 8;
-    const bool n256 = n % 256 == 0, n128 = n % 128 == 0;
-    const bool f32out = epi == ELIS_EPI_BIAS_RES_F32 || kResLnCode(epi);
-    int cfg = n128 ? 19 : 1;
-    if (!f32out && n256) {
-        cfg = 21;
-    } else if (f32out && n128) {
-        cfg = 32;
-        if (n256) {
-            const long long cus = device_cus();
-            const long long t256 = static_cast<long long>((m + 255) / 256) * (n / 256);
-            const long long t128 = static_cast<long long>((m + 127) / 128) * (n / 128);
-            const long long r256 = (t256 + cus - 1) / cus, r128 = (t128 + 2 * cus - 1) / (2 * cus);
-            if (r256 * 100 <= r128 * (k >= 2048 ? 60 : 53)) cfg = 21;
-        }
-    }
-    return launch_gemm_config(cfg, cfg == 1 ? 1 : kGroupM, x, w, bias, res, m, n, k, epi, out, st);
+    return launch_gemm_plan(plan_gemm(m, n, k, epi), x, w, bias, res, m, n, k, epi, out, st);
 }
 
 }  // namespace elis

@@ -208,7 +208,7 @@ size_t jobs_table_bytes(int max_jobs, int max_pos) {
 }
 
 JobTable jobs_table(void* base, int max_jobs, int max_pos) {
-    const size_t J = static_cast<size_t>(max_jobs), R = static_cast<size_t>(max_pos - 1);
+    const size_t J = static_cast<size_t>(max_jobs);
     char* p = static_cast<char*>(base);
     JobTable t;
     size_t o = 0;
@@ -229,34 +229,34 @@ JobTable jobs_table(void* base, int max_jobs, int max_pos) {
 }
 
 hipError_t launch_jobs_init(JobTable t, hipStream_t st) {
-    launch_kernel(jobs_init_kernel, grid_for(t.max_jobs > 0 ? t.max_jobs : 1), dim3(kThreads), 0, st, t);
-    return hipGetLastError();
+    ELIS_TRY(launch_kernel(jobs_init_kernel, grid_for(t.max_jobs > 0 ? t.max_jobs : 1), dim3(kThreads), 0, st, t));
+    return hipSuccess;
 }
 
 hipError_t launch_jobs_start(JobTable t, const int32_t* slots, const int64_t* arrival, int m, hipStream_t st) {
-    launch_kernel(jobs_start_kernel, grid_for(m), dim3(kThreads), 0, st, t, slots, arrival, m);
-    return hipGetLastError();
+    ELIS_TRY(launch_kernel(jobs_start_kernel, grid_for(m), dim3(kThreads), 0, st, t, slots, arrival, m));
+    return hipSuccess;
 }
 
 hipError_t launch_jobs_append(JobTable t, const int32_t* slots, const int32_t* off, const int32_t* tokens, int m,
                               int total, hipStream_t st) {
     if (total > 0)
-        launch_kernel(jobs_append_kernel, grid_for(total), dim3(kThreads), 0, st, t, slots, off, tokens, m,
-                           total);
-    launch_kernel(jobs_len_kernel, grid_for(m), dim3(kThreads), 0, st, t, slots, off, m);
-    return hipGetLastError();
+        ELIS_TRY(launch_kernel(jobs_append_kernel, grid_for(total), dim3(kThreads), 0, st, t, slots, off, tokens, m,
+                           total));
+    ELIS_TRY(launch_kernel(jobs_len_kernel, grid_for(m), dim3(kThreads), 0, st, t, slots, off, m));
+    return hipSuccess;
 }
 
 hipError_t launch_jobs_pack(JobTable t, const int32_t* slots, int n, int total, int max_seqlen, int32_t* ids,
                             int32_t* cu, hipStream_t st) {
-    launch_kernel(jobs_pack_scan_kernel, dim3(1), dim3(1024), 0, st, t, slots, n, total, max_seqlen, cu);
-    launch_kernel(jobs_pack_gather_kernel, grid_for(total), dim3(kThreads), 0, st, t, slots, n, total, cu, ids);
-    return hipGetLastError();
+    ELIS_TRY(launch_kernel(jobs_pack_scan_kernel, dim3(1), dim3(1024), 0, st, t, slots, n, total, max_seqlen, cu));
+    ELIS_TRY(launch_kernel(jobs_pack_gather_kernel, grid_for(total), dim3(kThreads), 0, st, t, slots, n, total, cu, ids));
+    return hipSuccess;
 }
 
 hipError_t launch_jobs_store_pred(JobTable t, const int32_t* slots, const float* pred, int n, hipStream_t st) {
-    launch_kernel(jobs_store_pred_kernel, grid_for(n), dim3(kThreads), 0, st, t, slots, pred, n);
-    return hipGetLastError();
+    ELIS_TRY(launch_kernel(jobs_store_pred_kernel, grid_for(n), dim3(kThreads), 0, st, t, slots, pred, n));
+    return hipSuccess;
 }
 
 size_t jobs_select_workspace_bytes(int max_active) {
@@ -275,13 +275,13 @@ hipError_t launch_jobs_select(JobTable t, const int32_t* slots, const float* wai
     int32_t* idx = reinterpret_cast<int32_t*>(p + align_up(4 * n) + align_up(8 * n));
     void* sel_ws = p + align_up(4 * n) + align_up(8 * n) + align_up(4 * n);
     // Bad slots are flagged in the table's status word: the select clears its own.
-    launch_kernel(jobs_gather_kernel, grid_for(a), dim3(kThreads), 0, st, t, slots, a, wait, aging, pred, arr,
-                       t.status);
+    ELIS_TRY(launch_kernel(jobs_gather_kernel, grid_for(a), dim3(kThreads), 0, st, t, slots, a, wait, aging, pred, arr,
+                       t.status));
     hipError_t e = launch_select(pred, arr, a, k, idx, out_count, sel_ws, st);
     if (e != hipSuccess) return e;
     const int kk = k < a ? k : a;
-    if (kk > 0) launch_kernel(jobs_map_kernel, grid_for(kk), dim3(kThreads), 0, st, slots, idx, out_count, kk, out_slots);
-    return hipGetLastError();
+    if (kk > 0) ELIS_TRY(launch_kernel(jobs_map_kernel, grid_for(kk), dim3(kThreads), 0, st, slots, idx, out_count, kk, out_slots));
+    return hipSuccess;
 }
 
 }  // namespace elis

@@ -50,9 +50,20 @@ constexpr int kEpiResLnFfn2 = 5;
 hipError_t launch_gemm(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
                        int k, int epi, void* out, hipStream_t st);
 
+// Launch plan of one product (gemm.hip): rows [0, m1) with configuration `main`, then, when
+// m1 < M, rows [m1, M) with configuration `rest`.
+struct GemmPlan {
+    int main, m1, rest;
+};
+GemmPlan plan_gemm(int m, int n, int k, int epi);
+hipError_t launch_gemm_plan(const GemmPlan& p, const uint16_t* x, const uint16_t* w, const float* bias,
+                            Residual res, int m, int n, int k, int epi, void* out, hipStream_t st);
+// Tile of a configuration (zeros if unknown) and the configuration of a tile (-1 if none).
+int gemm_config_of_tile(int bm, int bn, int wgs_per_cu);
+
 hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uint16_t* w, const float* bias,
                               Residual res, int m, int n, int k, int epi, void* out, hipStream_t st);
-int gemm_config_bn(int cfg);
+void gemm_config_tile(int cfg, int* bm, int* bn, int* wgs_per_cu);
 
 // attention.hip
 hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh,
@@ -116,12 +127,19 @@ hipError_t launch_jobs_select(JobTable t, const int32_t* slots, const float* wai
 // otherwise it returns false and leaves both null.
 bool launch_timing_events(hipEvent_t* start, hipEvent_t* stop);
 
+// Returns from the enclosing launcher with the first failing HIP status.
+#define ELIS_TRY(expr)                       \
+    do {                                     \
+        const hipError_t elis_e_ = (expr);   \
+        if (elis_e_ != hipSuccess) return elis_e_; \
+    } while (0)
+
 // Every kernel of the library is enqueued through launch_kernel. When the hook
 // hands out events they travel with the dispatch packet (hipExtLaunchKernel)
 // and take its own start and end timestamps, so timing a class puts no marker
 // packets, and no extra gaps, between the kernels of a forward pass.
 template <typename... P, typename... A>
-inline hipError_t launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t lds, hipStream_t st,
+[[nodiscard]] inline hipError_t launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t lds, hipStream_t st,
                                 A... a) {
     static_assert(sizeof...(P) == sizeof...(A), "kernel argument count");
     std::tuple<P...> args{static_cast<P>(a)...};

@@ -145,20 +145,20 @@ hipError_t launch_embed_ln(const int32_t* ids, const int32_t* cu, int n, int tot
                            int vocab, int max_pos, float eps, LnOut out, uint32_t* status, hipStream_t st) {
     const dim3 grid((total + kRowsPerBlock - 1) / kRowsPerBlock), block(kRowsPerBlock * kWave);
 #define CALL(V)                                                                                          \
-    launch_kernel(embed_ln_kernel<V>, grid, block, 0, st, ids, cu, n, total, word, pos, type0, g, b, d, \
-                       vocab, max_pos, eps, out, status)
+    ELIS_TRY(launch_kernel(embed_ln_kernel<V>, grid, block, 0, st, ids, cu, n, total, word, pos, type0, g, b, d, \
+                       vocab, max_pos, eps, out, status))
     ELIS_VPL_SWITCH(d, CALL)
 #undef CALL
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 hipError_t launch_layernorm(const float* x, const float* g, const float* b, int rows, int d, float eps,
                             LnOut out, hipStream_t st) {
     const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock), block(kRowsPerBlock * kWave);
-#define CALL(V) launch_kernel(layernorm_kernel<V>, grid, block, 0, st, x, g, b, rows, d, eps, out)
+#define CALL(V) ELIS_TRY(launch_kernel(layernorm_kernel<V>, grid, block, 0, st, x, g, b, rows, d, eps, out))
     ELIS_VPL_SWITCH(d, CALL)
 #undef CALL
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace elis

@@ -138,8 +138,8 @@ namespace {
 template <int ACT, bool POOLED>
 hipError_t fc(const float* in, const float* hidden, const float* z, const int32_t* start, int pooling, int n, int K,
               int N, const float* w, const float* b, float* out, hipStream_t st) {
-    launch_kernel((head_fc_kernel<ACT, POOLED>), dim3(N, (n + kFcSeq - 1) / kFcSeq), dim3(kWave), 0, st, in,
-                       hidden, z, start, pooling, n, K, N, w, b, out);
+    ELIS_TRY(launch_kernel((head_fc_kernel<ACT, POOLED>), dim3(N, (n + kFcSeq - 1) / kFcSeq), dim3(kWave), 0, st, in,
+                       hidden, z, start, pooling, n, K, N, w, b, out));
     return hipSuccess;
 }
 
@@ -160,9 +160,9 @@ hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int
     if (d % 4 != 0) return hipErrorInvalidValue;
     const dim3 cols(n, (d + kCols - 1) / kCols);
     if (pooling == ELIS_POOL_MEAN) {
-        launch_kernel(pool_partial_kernel, dim3(n, cols.y, scr.nchunk), dim3(kCols), 0, st, hidden, tab.start,
-                           tab.len, d, scr.nchunk, scr.partial);
-        launch_kernel(pool_reduce_kernel, cols, dim3(kCols), 0, st, scr.partial, tab.len, d, scr.nchunk, scr.z);
+        ELIS_TRY(launch_kernel(pool_partial_kernel, dim3(n, cols.y, scr.nchunk), dim3(kCols), 0, st, hidden, tab.start,
+                           tab.len, d, scr.nchunk, scr.partial));
+        ELIS_TRY(launch_kernel(pool_reduce_kernel, cols, dim3(kCols), 0, st, scr.partial, tab.len, d, scr.nchunk, scr.z));
     }
     const int hh = head.layers >= 2 ? head.hidden : 0;
     float* cur = scr.hid;
@@ -180,9 +180,9 @@ hipError_t launch_pool_head(const float* hidden, SeqTable tab, int n, int d, int
             nxt = t;
         }
     }
-    launch_kernel(head_out_kernel, dim3(n), dim3(kWave), 0, st, hidden, scr.z, tab.start, d, pooling, hh, cur,
-                       head.w2, head.b2, scale, shift, out);
-    return hipGetLastError();
+    ELIS_TRY(launch_kernel(head_out_kernel, dim3(n), dim3(kWave), 0, st, hidden, scr.z, tab.start, d, pooling, hh, cur,
+                       head.w2, head.b2, scale, shift, out));
+    return hipSuccess;
 }
 
 }  // namespace elis

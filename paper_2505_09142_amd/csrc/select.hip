@@ -641,31 +641,31 @@ hipError_t launch_select(const float* pred, const int64_t* arrival, int n, int k
     if (n < 1 || n > kLargeMaxN || k < 0) return hipErrorInvalidValue;
     uint32_t* status = static_cast<uint32_t*>(workspace);
     if (n <= kRankMaxN) {
-        launch_kernel(select_rank_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, n, k, out_idx, out_count,
-                           status);
-        return hipGetLastError();
+        ELIS_TRY(launch_kernel(select_rank_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, n, k, out_idx, out_count,
+                           status));
+        return hipSuccess;
     }
     if (n <= kSortMaxN) {
-        launch_kernel(select_sort_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, n, k, out_idx, out_count,
-                           status);
-        return hipGetLastError();
+        ELIS_TRY(launch_kernel(select_sort_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, n, k, out_idx, out_count,
+                           status));
+        return hipSuccess;
     }
     const int kk = k < n ? k : n;
     if (kk > kSortMaxN) return hipErrorInvalidValue;
     LargeWs ws;
     large_layout(n, &ws, static_cast<char*>(workspace));
-    launch_kernel(select_init_kernel, dim3(1), dim3(256), 0, st, ws, kk, out_count);
-    if (kk == 0) return hipGetLastError();
+    ELIS_TRY(launch_kernel(select_init_kernel, dim3(1), dim3(256), 0, st, ws, kk, out_count));
+    if (kk == 0) return hipSuccess;
     const dim3 grid(ws.groups), red(kReduceBlocks);
-    launch_kernel((select_count_kernel<21, 11>), grid, dim3(kBlock), 0, st, pred, n, ws);
-    launch_kernel((select_reduce_kernel<11>), red, dim3(1024), 0, st, ws);
-    launch_kernel((select_count_kernel<10, 11>), grid, dim3(kBlock), 0, st, pred, n, ws);
-    launch_kernel((select_reduce_kernel<11>), red, dim3(1024), 0, st, ws);
-    launch_kernel((select_count_kernel<0, 10>), grid, dim3(kBlock), 0, st, pred, n, ws);
-    launch_kernel((select_reduce_kernel<10>), red, dim3(1024), 0, st, ws);
-    launch_kernel(select_scatter_kernel, grid, dim3(kBlock), 0, st, pred, n, ws);
-    launch_kernel(select_final_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, kk, ws, out_idx);
-    return hipGetLastError();
+    ELIS_TRY(launch_kernel((select_count_kernel<21, 11>), grid, dim3(kBlock), 0, st, pred, n, ws));
+    ELIS_TRY(launch_kernel((select_reduce_kernel<11>), red, dim3(1024), 0, st, ws));
+    ELIS_TRY(launch_kernel((select_count_kernel<10, 11>), grid, dim3(kBlock), 0, st, pred, n, ws));
+    ELIS_TRY(launch_kernel((select_reduce_kernel<11>), red, dim3(1024), 0, st, ws));
+    ELIS_TRY(launch_kernel((select_count_kernel<0, 10>), grid, dim3(kBlock), 0, st, pred, n, ws));
+    ELIS_TRY(launch_kernel((select_reduce_kernel<10>), red, dim3(1024), 0, st, ws));
+    ELIS_TRY(launch_kernel(select_scatter_kernel, grid, dim3(kBlock), 0, st, pred, n, ws));
+    ELIS_TRY(launch_kernel(select_final_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, kk, ws, out_idx));
+    return hipSuccess;
 }
 
 }  // namespace elis

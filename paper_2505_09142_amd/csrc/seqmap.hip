@@ -73,9 +73,9 @@ __global__ __launch_bounds__(kThreads) void seqmap_kernel(const int32_t* __restr
 
 hipError_t launch_seqmap(const int32_t* cu, int n, int total, int max_seqlen, SeqTable tab, uint32_t* status,
                          hipStream_t st) {
-    launch_kernel(seqmap_kernel, dim3(1), dim3(kThreads), 0, st, cu, n, total, max_seqlen, tab.start,
-                       tab.len, tab.tile_off, status);
-    return hipGetLastError();
+    ELIS_TRY(launch_kernel(seqmap_kernel, dim3(1), dim3(kThreads), 0, st, cu, n, total, max_seqlen, tab.start,
+                       tab.len, tab.tile_off, status));
+    return hipSuccess;
 }
 
 }  // namespace elis

@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 from paper_2505_09142_amd import _elis as E
@@ -180,6 +181,60 @@ def test_building_blocks_reject_invalid_arguments(lib):
     assert E.elis_layernorm(FAKE, FAKE, FAKE, 4, 64, 1e-5, None, None, None) == E.ELIS_EINVAL
     assert E.elis_layernorm(FAKE, FAKE, FAKE, 4, 100, 1e-5, FAKE, None, None) == E.ELIS_EUNSUPPORTED
     assert E.elis_layernorm(FAKE, FAKE, FAKE, 0, 64, 1e-5, FAKE, None, None) == E.ELIS_EINVAL
+
+
+def test_linear_plan_host_only(lib):
+    """The launch plan of a product is host arithmetic: rows split at a whole number of main-tile
+    rows, the two launches cover [0, m), tiles of the shapes the library has, and the arguments
+    elis_linear rejects are rejected here too."""
+    tiles = {(64, 128), (128, 64), (128, 128), (256, 256)}
+    rng = np.random.default_rng(5)
+    splits = 0
+    for _ in range(400):
+        n = int(rng.choice([384, 512, 768, 1024, 2304, 3072, 4096, 320]))
+        k = int(rng.choice([64, 128, 768, 1024, 3072, 4096]))
+        m = int(rng.integers(1, 120000))
+        epi = int(rng.integers(0, 3))
+        st, (bm, bn, wg, m1, rbm, rbn, rwg) = E.elis_linear_plan(m, n, k, epi)
+        assert st == E.ELIS_OK
+        assert (bm, bn) in tiles and n % bn == 0 and wg in (1, 2)
+        assert 1 <= m1 <= m
+        if m1 < m:
+            splits += 1
+            assert m1 % bm == 0 and (rbm, rbn) in tiles and n % rbn == 0 and rwg in (1, 2)
+            assert (rbm, rbn, rwg) != (bm, bn, wg)
+            # the first launch fills whole rounds of work-group slots (256 CUs without a GPU): as
+            # many whole rows of tiles as fit in the full rounds of a single launch
+            per_row, slots = n // bn, wg * 256
+            full = (-(-m // bm) * per_row) // slots * slots
+            assert full >= slots and full - per_row < (m1 // bm) * per_row <= full
+        else:
+            assert (rbm, rbn, rwg) == (0, 0, 0)
+    assert splits > 20
+    assert E.elis_linear_plan(23931, 768, 3072, E.ELIS_EPI_BIAS_RES_F32)[1][3] < 23931
+    assert E.elis_linear_plan(0, 768, 768, 0)[0] == E.ELIS_EINVAL
+    assert E.elis_linear_plan(100, 100, 768, 0)[0] == E.ELIS_EUNSUPPORTED
+    assert E.elis_linear_plan(100, 768, 100, 0)[0] == E.ELIS_EUNSUPPORTED
+    assert E.elis_linear_plan(100, 768, 768, 3)[0] == E.ELIS_EINVAL
+
+
+def test_linear_with_plan_rejects_invalid_plans(lib):
+    FAKE = 256  # never dereferenced: every call below fails validation on the host
+    def call(plan, m=1000, n=768, k=768, epi=E.ELIS_EPI_BIAS_BF16):
+        return E.elis_linear_with_plan(FAKE, FAKE, FAKE, None, m, n, k, epi, plan, FAKE, None)
+    assert call(None) == E.ELIS_EINVAL
+    assert call((96, 128, 1, 1000, 0, 0, 0)) == E.ELIS_EINVAL        # unknown tile
+    assert call((256, 256, 2, 1000, 0, 0, 0)) == E.ELIS_EINVAL       # 256 x 256 runs one per CU
+    assert call((256, 256, 1, 1000, 0, 0, 0), n=640) == E.ELIS_EINVAL  # tile width must divide n
+    assert call((128, 128, 2, 0, 0, 0, 0)) == E.ELIS_EINVAL          # m1 >= 1
+    assert call((128, 128, 2, 1001, 0, 0, 0)) == E.ELIS_EINVAL       # m1 <= m
+    assert call((128, 128, 2, 1000, 64, 128, 1)) == E.ELIS_EINVAL    # no rest when m1 == m
+    assert call((128, 128, 2, 500, 64, 128, 1)) == E.ELIS_EINVAL     # m1 a multiple of main_bm
+    assert call((128, 128, 2, 512, 128, 128, 2)) == E.ELIS_EINVAL    # rest differs from main
+    assert call((128, 128, 2, 512, 0, 0, 0)) == E.ELIS_EINVAL        # rest missing
+    assert call((128, 64, 2, 1000, 0, 0, 0)) == E.ELIS_EINVAL        # 128 x 64 only for n = 64 mod 128
+    assert call((256, 256, 1, 512, 128, 64, 2), n=768) == E.ELIS_EINVAL
+    assert call((128, 128, 2, 1000, 0, 0, 0), n=100) == E.ELIS_EUNSUPPORTED
 
 
 def test_timing_api_host_only(lib):

@@ -312,6 +312,63 @@ def test_linear_large_m_sampled(epi):
         assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1.2 * acc_tol)
 
 
+def test_linear_split_plans_agree_bitwise():
+    """Products whose launch plans differ (one launch of 64 x 128, 128 x 128 or 256 x 256 tiles, or
+    large tiles over whole rounds plus a second launch of small tiles over the remaining rows) give
+    the same bits on the rows they share."""
+    rng = np.random.default_rng(78)
+    for n, k, epi, ms in ((768, 3072, E.ELIS_EPI_BIAS_RES_F32, (300, 5000, 23931, 30000)),
+                          (2304, 768, E.ELIS_EPI_BIAS_BF16, (700, 6000, 23931, 26000)),
+                          (3072, 768, E.ELIS_EPI_BIAS_GELU_BF16, (3000, 12000, 23931))):
+        plans = {m: E.elis_linear_plan(m, n, k, epi)[1] for m in ms}
+        assert len(set(plans.values())) >= 3, plans
+        assert any(p[3] < m for m, p in plans.items()), plans   # at least one split plan
+        m_max = max(ms)
+        note(f"linear split plans n={n} k={k} epi={epi} plans={plans}")
+        xb = f32_to_bf16_bits(rng.standard_normal((m_max, k), dtype=np.float32))
+        wb = f32_to_bf16_bits(rng.standard_normal((n, k), dtype=np.float32) * 0.05)
+        bias = (rng.standard_normal(n) * 0.1).astype(np.float32)
+        f32 = epi == E.ELIS_EPI_BIAS_RES_F32
+        res = rng.standard_normal((m_max, n), dtype=np.float32) if f32 else None
+        d_x, d_w, d_bias = dev(xb), dev(wb), dev(bias)
+        d_res = dev(res) if f32 else None
+        outs = {}
+        for m in ms:
+            out = torch.empty((m, n), dtype=torch.float32 if f32 else torch.int16, device="cuda")
+            ok(E.elis_linear(d_x.data_ptr(), d_w.data_ptr(), d_bias.data_ptr(), d_res.data_ptr() if f32 else None,
+                             m, n, k, epi, out.data_ptr(), stream()))
+            torch.cuda.synchronize()
+            outs[m] = out.cpu().numpy().view(np.uint32 if f32 else np.uint16)
+        ref = outs[m_max]
+        for m in ms:
+            assert np.array_equal(outs[m], ref[:m]), (m, plans[m])
+        # every tile configuration and split forced through elis_linear_with_plan: the same bits
+        m = m_max
+        forced = [(128, 128, 2, m, 0, 0, 0), (64, 128, 2, m, 0, 0, 0), (64, 128, 1, m, 0, 0, 0),
+                  (128, 128, 2, 8192, 64, 128, 1), (64, 128, 2, 4096, 128, 128, 2)]
+        if n % 256 == 0:
+            forced += [(256, 256, 1, m, 0, 0, 0), (256, 256, 1, 4096, 64, 128, 2), (256, 256, 1, 8192, 128, 128, 2)]
+        for plan in forced:
+            note(f"  forced plan {plan}")
+            out = torch.empty((m, n), dtype=torch.float32 if f32 else torch.int16, device="cuda")
+            ok(E.elis_linear_with_plan(d_x.data_ptr(), d_w.data_ptr(), d_bias.data_ptr(),
+                                       d_res.data_ptr() if f32 else None, m, n, k, epi, plan, out.data_ptr(), stream()))
+            torch.cuda.synchronize()
+            assert np.array_equal(out.cpu().numpy().view(np.uint32 if f32 else np.uint16), ref), plan
+        # and the largest against the fp64 product on sampled rows
+        rows = np.unique(np.concatenate([[0, m_max - 1], rng.integers(0, m_max, 200)]))
+        x64, w64 = bf16_to_f64(xb[rows]), bf16_to_f64(wb)
+        pre = x64 @ w64.T + bias
+        acc_tol = 1e-5 * (np.abs(x64) @ np.abs(w64).T) + 1e-6
+        if f32:
+            got = ref[rows].view(np.float32).astype(np.float64)
+            assert np.all(np.abs(got - (pre + res[rows])) <= acc_tol + 1e-6 * np.abs(pre + res[rows]))
+        else:
+            got = bf16_to_f64(ref[rows].view(np.uint16))
+            exp = oracle.gelu(pre) if epi == E.ELIS_EPI_BIAS_GELU_BF16 else pre
+            assert np.all(np.abs(got - exp) <= 2.0 ** -8 * np.abs(exp) + 1.2 * acc_tol)
+
+
 def test_linear_routes_agree_bitwise():
     """Shapes routed to different tile configurations accumulate every output element in the same
     order with the same instruction and the same epilogue arithmetic: a row (column) computed by
