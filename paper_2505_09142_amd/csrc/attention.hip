@@ -24,8 +24,8 @@
 //
 // LDS. K is stored row-major with 16-byte chunks XOR-swizzled by row pairs
 // (the 16 rows one fragment read touches then cover every bank once); V is
-// stored transposed (V^T[d][key], rows padded to 72 keys) so that a lane's
-// 8 keys for one d are two 8-byte reads. Two LDS buffers: the next tile is
+// stored transposed (V^T[d][key], rows padded to 72 keys, keys permuted within each
+// 32-key chunk, see vt_pos) so that a lane's 8 keys for one d are one 16-byte read. Two LDS buffers: the next tile is
 // fetched from HBM into registers while the current one is multiplied, so
 // each tile costs one barrier and its load latency is hidden.
 #include <math.h>
@@ -50,6 +50,14 @@ __device__ __forceinline__ int kswz(int row) {
     // 16 rows: rows start on 2 (d_head 64) or 4 (d_head 32) bank groups.
     constexpr int CPR = DH / 8;
     return CPR == 8 ? ((row >> 1) & 7) : ((row >> 2) & 3);
+}
+
+// Position of key k in a V^T row. The P^T operand of lane group g holds keys {4g..4g+3} and
+// {16+4g..16+4g+3} of each 32-key chunk (the accumulator layout of S^T); storing key
+// 32c + 16h + 4g + r at 32c + 8g + 4h + r puts the 8 keys of one operand in 16 contiguous bytes,
+// so a lane fetches its V^T operand with one 16-byte read. Pairs (2i, 2i+1) stay adjacent.
+__device__ __forceinline__ int vt_pos(int k) {
+    return (k & ~31) | (((k >> 2) & 3) << 3) | (((k >> 4) & 1) << 2) | (k & 3);
 }
 
 // Maximum over the lanes l, l^16, l^32, l^48 (the four lanes that hold one query's scores).
@@ -157,13 +165,14 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
             if (VCH % (kWaves * kWave) == 0 || u < VCH) {
                 const int tp = u % (kBKV / 2), ch = u / (kBKV / 2);
                 const u32x4 a = rv0[i], bb = rv1[i];
+                const int pos = vt_pos(2 * tp);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     // (key 2tp, key 2tp+1) pairs for d = 8ch+2e and 8ch+2e+1
                     const uint32_t lo = __builtin_amdgcn_perm(bb[e], a[e], 0x05040100u);
                     const uint32_t hi = __builtin_amdgcn_perm(bb[e], a[e], 0x07060302u);
-                    *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e) * kVtStride + 2 * tp]) = lo;
-                    *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e + 1) * kVtStride + 2 * tp]) = hi;
+                    *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e) * kVtStride + pos]) = lo;
+                    *reinterpret_cast<uint32_t*>(&v_s[(ch * 8 + 2 * e + 1) * kVtStride + pos]) = hi;
                 }
             }
         }
@@ -261,14 +270,8 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
             const int d = dt * 16 + r16;
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
-                const u32x2 lo = *reinterpret_cast<const u32x2*>(&v_s[d * kVtStride + kc * 32 + 4 * g]);
-                const u32x2 hi = *reinterpret_cast<const u32x2*>(&v_s[d * kVtStride + kc * 32 + 16 + 4 * g]);
-                u32x4 w;
-                w[0] = lo[0];
-                w[1] = lo[1];
-                w[2] = hi[0];
-                w[3] = hi[1];
-                const bf16x8 vf = __builtin_bit_cast(bf16x8, w);
+                // keys {kc*32 + 4g .. +3, kc*32 + 16 + 4g .. +3}: 16 contiguous bytes in V^T
+                const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&v_s[d * kVtStride + kc * 32 + 8 * g]);
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     o[dt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc][j], o[dt][j], 0, 0, 0);
