@@ -95,6 +95,7 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
     const int g = lane >> 4, r16 = lane & 15;
     const int qw = q0 + wid * kQPerWave;
+    const float lag = 8.0f / scale_log2;  // raw-score lag of the lazy running maximum
 
     // Query fragments (B operand of S^T = K Q^T): lane holds Q[query][8 d's of its k-group].
     bf16x8 qf[2][KS];
@@ -227,6 +228,13 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 
         // Online softmax. The running maximum is kept in raw-score units; the scale
         // log2(e)/sqrt(d_head) enters once per score through the FMA inside exp2.
+        // Lazy rescaling: the reference point m_run of a 16-query block only moves when one of
+        // its queries meets a score more than lag = 8 / scale_log2 above it; then every query
+        // of the block moves to its own running maximum and the block's accumulators are
+        // rescaled. In between, p = 2^((s - m_run) * scale_log2) <= 2^8, which bf16 and the
+        // fp32 sums hold with the same relative precision, and nothing is rescaled: after the
+        // first tile a block rarely rescales again (with an exact running maximum nearly every
+        // tile raised some query's maximum).
         bf16x8 pf[2][2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
@@ -235,24 +243,21 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
             for (int tt = 1; tt < 4; ++tt)
                 mx = fmaxf(mx, fmaxf(fmaxf(sc[tt][j][0], sc[tt][j][1]), fmaxf(sc[tt][j][2], sc[tt][j][3])));
             mx = quad_max(mx);
-            const float m_new = fmaxf(m_run[j], mx);
-            // alpha < 1 only where this tile raised the running maximum; once the maximum
-            // has settled (the common case after the first tiles) the whole wave skips the
-            // rescale of its output accumulators.
-            const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_new) * scale_log2);
-            const bool rescale = __builtin_amdgcn_ballot_w64(m_new != m_run[j]) != 0;
-            m_run[j] = m_new;
-            const float nb = -m_new * scale_log2;
+            // m_run = -inf on the first tile: every query grows (each tile holds a valid key).
+            if (__builtin_amdgcn_ballot_w64(mx > m_run[j] + lag) != 0) {
+                const float m_new = fmaxf(m_run[j], mx);
+                const float alpha = __builtin_amdgcn_exp2f((m_run[j] - m_new) * scale_log2);
+                m_run[j] = m_new;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) o[dt][j] *= alpha;
+                lsum[j] *= alpha;
+            }
+            const float nb = -m_run[j] * scale_log2;
             float p[4][4];
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) p[tt][r] = __builtin_amdgcn_exp2f(fmaf(sc[tt][j][r], scale_log2, nb));
-            if (rescale) {
-#pragma unroll
-                for (int dt = 0; dt < DT; ++dt) o[dt][j] *= alpha;
-                lsum[j] *= alpha;
-            }
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
                 u32x4 w;
