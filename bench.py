@@ -53,19 +53,27 @@ def _describe(w):
 
 
 def _algorithmic(w, b):
-    """Per-launch algorithmic FLOPs (contractions) or bytes (row kernels) by kernel class."""
+    """Algorithmic FLOPs (contractions) or bytes (row kernels) by kernel class: (kind, average per
+    launch, launches per step). With CLS pooling the last layer needs, after its QKV product, only
+    the CLS rows (one attention query and one row of every later product per sequence); that is
+    all the library computes there, and all that is counted."""
     s = w.shape
     T, n, d, F, L = b.total, b.n, s.d_model, s.d_ff, s.n_layers
-    sumsq = float((b.lengths.astype(float) ** 2).sum())
+    lens = b.lengths.astype(float)
+    sumsq = float((lens ** 2).sum())
+    cls_tail = s.pooling == 0 and L > 0
+    rows = (L - 1) * T + n if cls_tail else L * T          # rows through the post-attention layers
+    att = 4.0 * d * ((L - 1) * sumsq + float(lens.sum())) if cls_tail else 4.0 * d * L * sumsq
+    # fp32 row in; bf16 row + (mean, rstd) out (the last LayerNorm writes an fp32 row instead:
+    # counted as the common case)
+    ln_row = d * (4.0 + 2.0) + 8.0
     return {
         "gemm_qkv": ("flop", 2.0 * T * d * 3 * d, L),
-        "attention": ("flop", 4.0 * sumsq * d, L),
-        "gemm_o": ("flop", 2.0 * T * d * d, L),
-        "gemm_ffn1": ("flop", 2.0 * T * d * F, L),
-        "gemm_ffn2": ("flop", 2.0 * T * F * d, L),
-        # fp32 row in; bf16 row + (mean, rstd) out (the last LayerNorm writes an fp32 row instead:
-        # counted as the common case)
-        "layernorm": ("byte", T * (d * (4.0 + 2.0) + 8.0), 2 * L),
+        "attention": ("flop", att / L, L),
+        "gemm_o": ("flop", 2.0 * rows * d * d / L, L),
+        "gemm_ffn1": ("flop", 2.0 * rows * d * F / L, L),
+        "gemm_ffn2": ("flop", 2.0 * rows * F * d / L, L),
+        "layernorm": ("byte", 2 * rows * ln_row / (2 * L), 2 * L),
         # ids + gathered bf16 word and position rows in; fp32 pre-norm + bf16 rows + stats out
         "embed_ln": ("byte", T * (4.0 + d * (2.0 + 2.0 + 4.0 + 2.0) + 8.0), 1),
         # the hidden rows pooling reads (CLS: one per sequence; mean: every token) + every head weight once
@@ -107,28 +115,37 @@ def _gemm_kernel(bm, bn, wgs, epi, n, f32):
 
 
 def class_kernels(workload: str) -> dict:
-    """class -> ([kernel names, one per launch of the class], sources)."""
+    """class -> (kernel names any launch of the class dispatches, sources, launches per pass).
+    A GEMM class uses the plan at T rows (one or two kernels) and, with CLS pooling, the plan at
+    n rows in the last layer; the out-projection of that layer also gathers its residual rows."""
     from paper_2505_09142_amd import _elis as E
     from workloads import WORKLOADS, make_batch
     w = WORKLOADS[workload]
     s = w.shape
-    T, d, F = make_batch(w).total, s.d_model, s.d_ff
+    b = make_batch(w)
+    T, n, d, F, L = b.total, b.n, s.d_model, s.d_ff, s.n_layers
+    cls_tail = s.pooling == 0 and L > 0
     dims = {"gemm_qkv": (3 * d, d), "gemm_o": (d, d), "gemm_ffn1": (F, d), "gemm_ffn2": (d, F)}
     out = {}
-    for cls, (n, k) in dims.items():
+    for cls, (nn, k) in dims.items():
         pub, internal = _GEMM_EPI[cls]
-        st, (bm, bn, wg, m1, rbm, rbn, rwg) = E.elis_linear_plan(T, n, k, pub)
-        if st != 0:
-            raise SystemExit(f"elis_linear_plan failed for {cls}: {st}")
-        names = [_gemm_kernel(bm, bn, wg, internal, n, pub == 2)]
-        if m1 < T:
-            names.append(_gemm_kernel(rbm, rbn, rwg, internal, n, pub == 2))
-        out[cls] = (names, _GEMM_SRC)
+        names = []
+        for m in ([T, n] if cls_tail and cls != "gemm_qkv" else [T]):
+            st, (bm, bn, wg, m1, rbm, rbn, rwg) = E.elis_linear_plan(m, nn, k, pub)
+            if st != 0:
+                raise SystemExit(f"elis_linear_plan failed for {cls}: {st}")
+            for kname in [_gemm_kernel(bm, bn, wg, internal, nn, pub == 2)] + (
+                    [_gemm_kernel(rbm, rbn, rwg, internal, nn, pub == 2)] if m1 < m else []):
+                if kname not in names:
+                    names.append(kname)
+        if cls == "gemm_o" and cls_tail:
+            names.append("gather_rows_kernel")
+        out[cls] = (names, _GEMM_SRC, L)
     vpl = (d + 255) // 256
     out["attention"] = ([f"attention_kernel<{d // s.n_heads}>"], ["paper_2505_09142_amd/csrc/attention.hip",
-                                                                  "paper_2505_09142_amd/csrc/common.h"])
+                                                                  "paper_2505_09142_amd/csrc/common.h"], L)
     out["layernorm"] = ([f"layernorm_kernel<{vpl}>"], ["paper_2505_09142_amd/csrc/norm.hip",
-                                                        "paper_2505_09142_amd/csrc/common.h"])
+                                                        "paper_2505_09142_amd/csrc/common.h"], 2 * L)
     return out
 
 
@@ -177,16 +194,23 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, workload, commands):
     cw = sorted(write[COPY_KERNEL])[-3:]
     f_scale = nbytes / (sum(cf) / len(cf) * 1024)
     w_scale = nbytes / (sum(cw) / len(cw) * 1024)
-    T, d, F = b.total, w.shape.d_model, w.shape.d_ff
+    T, n, d, F, L = b.total, b.n, w.shape.d_model, w.shape.d_ff, w.shape.n_layers
+    cls_tail = w.shape.pooling == 0 and L > 0
+
+    def mand(r):  # bytes a launch over r rows must move at least once: operands in, results out
+        return {
+            "gemm_o": r * d * 2 + d * d * 2 + d * 4 * 3 + r * 8 + r * d * 4 * 2,
+            "layernorm": r * (d * (4 + 2) + 8),
+            "gemm_ffn1": r * d * 2 + F * d * 2 + F * 4 + r * F * 2,
+            "gemm_ffn2": r * F * 2 + F * d * 2 + d * 4 * 3 + r * 8 + r * d * 4 * 2,
+        }
+    full, tail = mand(T), mand(n if cls_tail else T)
     qkv_b = T * 3 * d * 2
-    mandatory = {  # bytes a launch must move at least once: operands in, results out
-        "gemm_qkv": T * d * 2 + 3 * d * d * 2 + 3 * d * 4 + qkv_b,
-        "attention": qkv_b + T * d * 2,
-        "gemm_o": T * d * 2 + d * d * 2 + d * 4 * 3 + T * 8 + T * d * 4 * 2,
-        "layernorm": T * (d * (4 + 2) + 8),
-        "gemm_ffn1": T * d * 2 + F * d * 2 + F * 4 + T * F * 2,
-        "gemm_ffn2": T * F * 2 + F * d * 2 + d * 4 * 3 + T * 8 + T * d * 4 * 2,
-    }
+    mandatory = {c: ((L - 1) * full[c] + tail[c]) / L for c in full}  # average over the layers
+    mandatory["gemm_qkv"] = T * d * 2 + 3 * d * d * 2 + 3 * d * 4 + qkv_b
+    att_tail = (qkv_b * 2 // 3 + n * d * 2 * 2) if cls_tail else qkv_b + T * d * 2
+    mandatory["attention"] = ((L - 1) * (qkv_b + T * d * 2) + att_tail) / L
+    passes = len(fetch.get("seqmap_kernel", []))
     lines = [f"# HBM traffic per launch: {workload} (T = {T:,}), rocprofv3 PMC byte counters", "",
              "Two passes over the same bench command, one counter each (GPU box, repo root as working tree):", ""]
     lines += [f"    {c}" for c in commands]
@@ -195,20 +219,21 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, workload, commands):
               f"{', '.join(f'{v:.0f}' for v in cf)} KiB, WRITE_SIZE {', '.join(f'{v:.0f}' for v in cw)} KiB, "
               f"for {nbytes / 1024:.0f} KiB moved each way, so bytes = FETCH_SIZE x 1024 x {f_scale:.4f} "
               f"and WRITE_SIZE x 1024 x {w_scale:.4f}.", "",
-              "| class | kernels (one dispatch each per launch) | launches | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled MB | mandatory MB | ratio |",
+              "| class | kernels | launches | FETCH_SIZE KiB / launch | WRITE_SIZE KiB / launch | scaled MB / launch | mandatory MB / launch | ratio |",
               "|---|---|---:|---:|---:|---:|---:|---:|"]
     recs = {}
-    for cls, (knames, srcs) in class_kernels(workload).items():
+    for cls, (knames, srcs, lpp) in class_kernels(workload).items():
         label = " + ".join(f"`{k}`" for k in knames)
         fvs, wvs = [fetch.get(k, []) for k in knames], [write.get(k, []) for k in knames]
-        if not all(fvs) or not all(wvs):
+        if not passes or not all(fvs) or not all(wvs):
             lines.append(f"| {cls} | {label} | 0 | - | - | - | - | - |")
             continue
-        # per class launch: the sum of its kernels' per-dispatch averages
-        fk = sum(sum(v) / len(v) for v in fvs)
-        wk = sum(sum(v) / len(v) for v in wvs)
+        # per class launch: every dispatch of the class's kernels over the passes, / launches
+        launches = passes * lpp
+        fk = sum(sum(v) for v in fvs) / launches
+        wk = sum(sum(v) for v in wvs) / launches
         tb = fk * 1024 * f_scale + wk * 1024 * w_scale
-        lines.append(f"| {cls} | {label} | {len(fvs[0])} | {fk:,.0f} | {wk:,.0f} | {tb / 1e6:,.1f} | "
+        lines.append(f"| {cls} | {label} | {launches} | {fk:,.0f} | {wk:,.0f} | {tb / 1e6:,.1f} | "
                      f"{mandatory[cls] / 1e6:,.1f} | {tb / mandatory[cls]:.2f} |")
         recs[cls] = {"per_launch_bytes": tb, "fetch_kib": fk, "write_kib": wk, "fetch_scale": f_scale,
                      "write_scale": w_scale, "mandatory_bytes": mandatory[cls], "kernels": knames,
@@ -243,20 +268,20 @@ def summarize_mfma(csv_path, bench_json, command):
              "the kernel's busy cycles in which an average SIMD's matrix core was working. `algorithmic` = "
              "bench.py's FLOPs ÷ kernel time ÷ 2.5 PFLOP/s from the same run; the ratio algorithmic / busy is "
              "(clock under load) ÷ 2.4 GHz when the matrix cores run at their full rate while busy.", "",
-             "| class | kernels | launches | MFMA busy | algorithmic | algorithmic / busy |",
+             "| class | kernels | dispatches | MFMA busy | algorithmic | algorithmic / busy |",
              "|---|---|---:|---:|---:|---:|"]
-    for cls, (knames, _) in class_kernels(rec["config"]["workload"].split(":")[0]).items():
+    for cls, (knames, _, _) in class_kernels(rec["config"]["workload"].split(":")[0]).items():
         vs = [vals.get(k) for k in knames]
         if not all(v and v.get("SQ_VALU_MFMA_BUSY_CYCLES") for v in vs):
             continue
-        # cycles of a class launch: the sum over its kernels of their per-dispatch averages
-        mb = sum(sum(v["SQ_VALU_MFMA_BUSY_CYCLES"]) / len(v["SQ_VALU_MFMA_BUSY_CYCLES"]) for v in vs)
-        bc = sum(sum(v["SQ_BUSY_CYCLES"]) / len(v["SQ_BUSY_CYCLES"]) for v in vs)
+        # cycles summed over every dispatch of the class's kernels
+        mb = sum(sum(v["SQ_VALU_MFMA_BUSY_CYCLES"]) for v in vs)
+        bc = sum(sum(v["SQ_BUSY_CYCLES"]) for v in vs)
         busy = mb / simds / (bc / ses)
         k = rec["kernels"].get(cls, {})
         alg = k.get("tflops", 0.0) / PEAK_BF16_TFLOPS if "tflops" in k else None
         label = " + ".join(f"`{x}`" for x in knames)
-        lines.append(f"| {cls} | {label} | {len(vs[0]['SQ_BUSY_CYCLES'])} | {busy:.3f} | "
+        lines.append(f"| {cls} | {label} | {sum(len(v['SQ_BUSY_CYCLES']) for v in vs)} | {busy:.3f} | "
                      + (f"{alg:.3f} | {alg / busy:.2f} |" if alg is not None and busy > 0 else "- | - |"))
     with open(MFMA_PROFILE, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -276,17 +301,20 @@ def summarize_trace(stats_csv, command, bench_json):
     rec = json.loads(open(bench_json).read().strip().splitlines()[-1])
     roles = dict(_ROLES)
     ck = class_kernels(rec["config"]["workload"].split(":")[0])
-    roles.update({k: c for c, (ks, _) in ck.items() for k in ks})
-    rows, avg = [], {}
+    roles.update({k: c for c, (ks, _, _) in ck.items() for k in ks})
+    rows, tot, calls = [], {}, {}
     with open(stats_csv) as f:
         for r in csv.DictReader(f):
             n = re.sub(r"\(.*", "", r["Name"].replace("elis::(anonymous namespace)::", "").replace("void ", "")).strip()
-            avg[n] = float(r["AverageNs"]) / 1e3
+            tot[n] = float(r["TotalDurationNs"]) / 1e3
+            calls[n] = int(r["Calls"])
             rows.append(f"| `{n}` | {roles.get(n, '')} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e3:.1f} | "
                         f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
     rl = rec["roofline"]
     dom = rl["kernel"]
-    prof_us = sum(avg.get(k, 0.0) for k in ck[dom][0]) if dom in ck and all(k in avg for k in ck[dom][0]) else None
+    passes = calls.get("seqmap_kernel", 0)
+    prof_us = (sum(tot.get(k, 0.0) for k in ck[dom][0]) / (passes * ck[dom][2])
+               if dom in ck and passes and all(k in tot for k in ck[dom][0]) else None)
     cfg = rec["config"]
     steps, warm = rec["steps"], rec["warmup"]
     lines = [f"# Kernel trace: {cfg['workload'].split(':')[0]} (T = {cfg['total_tokens']:,}), predict + select", "",
@@ -298,7 +326,7 @@ def summarize_trace(stats_csv, command, bench_json):
     lines += ["", f"bench.py's own line in that run: {rec['ms_per_step']:.3f} ms per step, {rec['value']:.0f} seqs/s. "
               f"Dominant class `{dom}`: {rl['avg_launch_us']:.1f} µs per launch by bench.py's live HIP events "
               f"({rl['launches']} sampled launches, every {rl.get('timing_stride', 1)}th) vs "
-              + (f"{prof_us:.1f} µs" if prof_us else "n/a") + " (rocprofv3 averages above, summed over the class's kernels); "
+              + (f"{prof_us:.1f} µs" if prof_us else "n/a") + " (rocprofv3: the class's kernels' total time / its launches); "
               f"{rl['per_launch_flop'] / 1e9:.1f} GFLOP per launch -> {rl['achieved']:.0f} {rl['unit']} = "
               f"{100 * rl['frac']:.1f}% of the {rl['peak']:.0f} {rl['unit']} dense bf16 peak."]
     with open(TRACE_PROFILE, "w") as f:

@@ -270,6 +270,13 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
     // LayerNorm parameters of the row held in hb/sb (the input of the next layer).
     const float* prev_g = w->emb_ln_g;
     const float* prev_b = w->emb_ln_b;
+    // With CLS pooling and no hidden-state output only the CLS rows of the last layer reach the
+    // head: after that layer's QKV product (keys and values of every token), attention, the
+    // out-projection, the feed-forward block and both LayerNorms run on the n CLS rows alone.
+    // Every kernel computes a row independently of the others (attention a query), so the
+    // predictions are bit-identical to the full pass.
+    const bool cls_tail = c.pooling == ELIS_POOL_CLS && !out_hidden && L > 0;
+    const float* head_in = final32;
     for (int l = 0; l < L; ++l) {
         const elis_layer_weights& y = w->layers[l];
         const bool last = (l == L - 1);
@@ -277,6 +284,42 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
             return launch_gemm(xb, y.w_qkv, y.b_qkv, Residual{}, T, 3 * d, d, ELIS_EPI_BIAS_BF16, qkv, st);
         });
         if (e != hipSuccess) return status_of(e);
+        if (last && cls_tail) {
+            // One row per sequence, in buffers the full-size layer no longer needs:
+            //   attn <- CLS attention rows;  ha/sa <- the residual rows (hb/sb at each start);
+            //   x32/sb <- attention sub-block pre-norm rows and stats;  xb, ffn as usual;
+            //   ha <- FFN pre-norm rows;  hb <- final hidden rows.
+            e = timed(ELIS_K_ATTENTION, [&] {
+                return launch_attention(qkv, tab, n, T, c.n_heads, d / c.n_heads, attn, st, true);
+            });
+            if (e != hipSuccess) return status_of(e);
+            e = timed(ELIS_K_GEMM_O, [&] {
+                ELIS_TRY(launch_gather_rows(hb, sb, tab.start, n, d, ha, sa, st));
+                return launch_gemm(attn, y.w_o, y.b_o, Residual{ha, sa, prev_g, prev_b}, n, d, d, kEpiResLn, x32,
+                                   st);
+            });
+            if (e != hipSuccess) return status_of(e);
+            e = timed(ELIS_K_LAYERNORM, [&] {
+                return launch_layernorm(x32, y.ln1_g, y.ln1_b, n, d, c.ln_eps, LnOut{nullptr, xb, nullptr, sb}, st);
+            });
+            if (e != hipSuccess) return status_of(e);
+            e = timed(ELIS_K_GEMM_FFN1, [&] {
+                return launch_gemm(xb, y.w_1, y.b_1, Residual{}, n, F, d, ELIS_EPI_BIAS_GELU_BF16, ffn, st);
+            });
+            if (e != hipSuccess) return status_of(e);
+            e = timed(ELIS_K_GEMM_FFN2, [&] {
+                return launch_gemm(ffn, y.w_2, y.b_2, Residual{x32, sb, y.ln1_g, y.ln1_b}, n, d, F, kEpiResLnFfn2,
+                                   ha, st);
+            });
+            if (e != hipSuccess) return status_of(e);
+            e = timed(ELIS_K_LAYERNORM, [&] {
+                return launch_layernorm(ha, y.ln2_g, y.ln2_b, n, d, c.ln_eps, LnOut{hb, nullptr, nullptr, nullptr},
+                                        st);
+            });
+            if (e != hipSuccess) return status_of(e);
+            head_in = hb;
+            break;
+        }
         e = timed(ELIS_K_ATTENTION,
                   [&] { return launch_attention(qkv, tab, n, T, c.n_heads, d / c.n_heads, attn, st); });
         if (e != hipSuccess) return status_of(e);
@@ -312,7 +355,8 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
                               c.head_layers > 2 ? hid + static_cast<size_t>(n) * c.head_hidden : nullptr, p.nchunk};
         const HeadSpec head{c.head_layers, c.head_hidden, c.head_act, w->head_w1, w->head_b1, w->head_w2,
                             w->head_b2, w->head_mid_w, w->head_mid_b};
-        return launch_pool_head(final32, tab, n, d, c.pooling, head, c.out_scale, c.out_shift, out_pred, scr, st);
+        const SeqTable rows{cls_tail ? nullptr : tab.start, tab.len, tab.tile_off};
+        return launch_pool_head(head_in, rows, n, d, c.pooling, head, c.out_scale, c.out_shift, out_pred, scr, st);
     });
     return status_of(e);
 }

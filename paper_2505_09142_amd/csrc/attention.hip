@@ -74,7 +74,7 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                                                                   const int32_t* __restrict__ seq_len,
                                                                   const int32_t* __restrict__ tile_off, int n,
                                                                   int H, uint16_t* __restrict__ out,
-                                                                  float scale_log2) {
+                                                                  float scale_log2, int cls_only) {
     constexpr int CPR = DH / 8;   // 16-byte chunks per head row
     constexpr int KS = DH / 32;   // MFMA k-steps over d_head
     constexpr int DT = DH / 16;   // 16-wide d blocks of the output
@@ -82,10 +82,14 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     __shared__ __attribute__((aligned(16))) uint16_t sVt[2 * DH * kVtStride];
 
     const int tile = blockIdx.x, h = blockIdx.y;
-    if (tile >= tile_off[n]) return;  // uniform over the work-group
-    const int s = find_segment(tile_off, n, tile);
+    // cls_only: one work-group per (sequence, head) computing the first 32 queries (wave 0,
+    // exactly as in the full launch, so the CLS query sees the same arithmetic) and writing the
+    // CLS row alone, to row s of a one-row-per-sequence output.
+    if (cls_only ? tile >= n : tile >= tile_off[n]) return;  // uniform over the work-group
+    const int s = cls_only ? tile : find_segment(tile_off, n, tile);
     const int seq0 = seq_start[s], L = seq_len[s];
-    const int q0 = (tile - tile_off[s]) * kBQ;
+    const int q0 = cls_only ? 0 : (tile - tile_off[s]) * kBQ;
+    const int q_end = cls_only ? (L < kQPerWave ? L : kQPerWave) : L;  // queries computed
 
     const int D = H * DH, D3 = 3 * D;
     const uint16_t* Qg = qkv + h * DH;
@@ -192,7 +196,7 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
         const uint16_t* k_s = sK + b * (kBKV * DH);
         const uint16_t* v_s = sVt + b * (DH * kVtStride);
 
-        if (qw >= L) continue;  // this wave's queries are all past the end (uniform per wave)
+        if (qw >= q_end) continue;  // this wave's queries are all past the end (uniform per wave)
 
         // S^T = K Q^T: 4 key blocks x 2 query blocks (raw scores, unscaled).
         f32x4 sc[4][2];
@@ -293,8 +297,8 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     for (int j = 0; j < 2; ++j) {
         const float inv = 1.0f / lsum[j][0];
         const int qi = qw + j * 16 + r16;
-        if (qi >= L) continue;
-        uint16_t* orow = out + static_cast<size_t>(seq0 + qi) * D + h * DH;
+        if (cls_only ? qi != 0 : qi >= L) continue;
+        uint16_t* orow = out + static_cast<size_t>(cls_only ? s : seq0 + qi) * D + h * DH;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             u32x2 pk;
@@ -308,17 +312,17 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 }  // namespace
 
 hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh, uint16_t* out,
-                            hipStream_t st) {
+                            hipStream_t st, bool cls_only) {
     // Upper bound of sum_s ceil(len_s / kBQ); surplus work-groups exit at once.
-    const int tiles = (total + kBQ - 1) / kBQ + n;
+    const int tiles = cls_only ? n : (total + kBQ - 1) / kBQ + n;
     const dim3 grid(tiles, heads), block(kWaves * kWave);
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
     if (dh == 64)
         ELIS_TRY(launch_kernel(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2));
+                           out, scale_log2, cls_only ? 1 : 0));
     else if (dh == 32)
         ELIS_TRY(launch_kernel(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2));
+                           out, scale_log2, cls_only ? 1 : 0));
     else
         return hipErrorInvalidValue;
     return hipSuccess;

@@ -30,6 +30,9 @@ hipError_t launch_embed_ln(const int32_t* ids, const int32_t* cu, int n, int tot
                            LnOut out, uint32_t* status, hipStream_t st);
 hipError_t launch_layernorm(const float* x, const float* g, const float* b, int rows, int d, float eps,
                             LnOut out, hipStream_t st);
+// dst[s] = src[start[s]] and dst_stats[s] = src_stats[start[s]] for s < n (rows of d floats).
+hipError_t launch_gather_rows(const float* src, const float2* src_stats, const int32_t* start, int n, int d,
+                              float* dst, float2* dst_stats, hipStream_t st);
 
 // gemm.hip
 // Residual added by the fp32-output epilogues: the fp32 matrix x itself (stats null), or the
@@ -66,8 +69,9 @@ hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uin
 void gemm_config_tile(int cfg, int* bm, int* bn, int* wgs_per_cu);
 
 // attention.hip
+// cls_only: only the first query of each sequence, written to row s of out ([n, heads * dh]).
 hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh,
-                            uint16_t* out, hipStream_t st);
+                            uint16_t* out, hipStream_t st, bool cls_only = false);
 
 // pool_head.hip
 constexpr int kPoolChunk = 64;  // rows per partial sum of mean pooling

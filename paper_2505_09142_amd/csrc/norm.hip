@@ -125,7 +125,28 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void layernorm_kernel(const f
     ln_finish<VPL>(v, lane, d, g, b, eps, static_cast<size_t>(r), out);
 }
 
+// One wave per gathered row: float4 lanes across the row, lane 0 also copies the statistics.
+__global__ __launch_bounds__(kRowsPerBlock* kWave) void gather_rows_kernel(
+    const float* __restrict__ src, const float2* __restrict__ src_stats, const int32_t* __restrict__ start, int n,
+    int d, float* __restrict__ dst, float2* __restrict__ dst_stats) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int s = blockIdx.x * kRowsPerBlock + (threadIdx.x / kWave);
+    if (s >= n) return;
+    const size_t from = static_cast<size_t>(start[s]) * d, to = static_cast<size_t>(s) * d;
+    for (int e = 4 * lane; e < d; e += 4 * kWave)
+        *reinterpret_cast<f32x4*>(dst + to + e) = *reinterpret_cast<const f32x4*>(src + from + e);
+    if (lane == 0) dst_stats[s] = src_stats[start[s]];
+}
+
 }  // namespace
+
+hipError_t launch_gather_rows(const float* src, const float2* src_stats, const int32_t* start, int n, int d,
+                              float* dst, float2* dst_stats, hipStream_t st) {
+    if (n < 1 || d % 4 != 0) return hipErrorInvalidValue;
+    ELIS_TRY(launch_kernel(gather_rows_kernel, dim3((n + kRowsPerBlock - 1) / kRowsPerBlock),
+                           dim3(kRowsPerBlock * kWave), 0, st, src, src_stats, start, n, d, dst, dst_stats));
+    return hipSuccess;
+}
 
 #define ELIS_VPL_SWITCH(d, CALL)          \
     switch ((d + 255) / 256) {            \

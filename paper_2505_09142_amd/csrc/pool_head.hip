@@ -74,7 +74,10 @@ __global__ __launch_bounds__(kCols) void pool_reduce_kernel(const float* __restr
 
 __device__ __forceinline__ const float* pooled_row(int s, int pooling, const float* hidden, const float* z,
                                                    const int32_t* start, int d) {
-    return pooling == ELIS_POOL_CLS ? hidden + static_cast<size_t>(start[s]) * d : z + static_cast<size_t>(s) * d;
+    // CLS pooling: the sequence's first row, or row s when the hidden rows are one per sequence
+    // (start null: the encoder's last layer ran on the CLS rows only).
+    const size_t row = start ? static_cast<size_t>(start[s]) : static_cast<size_t>(s);
+    return pooling == ELIS_POOL_CLS ? hidden + row * d : z + static_cast<size_t>(s) * d;
 }
 
 // One fully connected layer of the head, out[s, j] = act(x[s, :] . w[j, :] + b[j]), K inputs,

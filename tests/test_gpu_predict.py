@@ -262,3 +262,23 @@ def test_timing_stride_samples_class_launches():
         assert ms > 0
     assert E.elis_timing_read(E.K["gemm_qkv"])[1] == 0
     E.elis_timing_reset()
+
+
+@pytest.mark.parametrize("w", [W_TINY, W_TINY_CLS_LIN8, W_BERT_B64, W_TINY_HEAD8], ids=lambda w: w.name)
+def test_cls_tail_is_bit_identical(w):
+    """Without a hidden-state output and with CLS pooling, the last layer runs on the CLS rows
+    only (after its full QKV product); the predictions must equal the full pass bit for bit.
+    Mean pooling (tiny_head8) always runs the full pass: both calls agree there too."""
+    note(f"CLS-only last layer vs full pass: {w.name}")
+    _, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    p_full, h_full, _ = run(pr, b, want_hidden=True)
+    p_tail, h_tail, _ = run(pr, b, want_hidden=False)
+    assert h_tail is None and h_full is not None
+    assert np.array_equal(p_full.view(np.uint32), p_tail.view(np.uint32))
+    if w.shape.pooling == 0:
+        # and a batch of length-1 sequences (n = T: the one-row-per-sequence buffers are full-size)
+        ones = pack([b.seq(s)[:1] for s in range(b.n)])
+        p1, _, _ = run(pr, ones, want_hidden=True)
+        p2, _, _ = run(pr, ones, want_hidden=False)
+        assert np.array_equal(p1.view(np.uint32), p2.view(np.uint32))
