@@ -282,3 +282,48 @@ def test_cls_tail_is_bit_identical(w):
         p1, _, _ = run(pr, ones, want_hidden=True)
         p2, _, _ = run(pr, ones, want_hidden=False)
         assert np.array_equal(p1.view(np.uint32), p2.view(np.uint32))
+
+
+def test_hip_graph_replay_matches_eager():
+    """elis_predict_remaining + elis_isrtf_select only enqueue kernels (no allocation, memset or
+    synchronisation), so a round can be captured into a HIP graph. Every replay, with eager
+    library work and synchronisations between replays, must give the eager results bit for bit."""
+    w = W_BERT_B64
+    note("HIP graph capture of predict + select (bert_base_b64)")
+    _, pr = predictor(w.shape, w.weight_seed)
+    b = make_batch(w)
+    ids, cu, arr = upload_batch(b)
+    other = make_batch(dataclasses.replace(w, data_seed=w.data_seed + 5))
+    o_ids, o_cu, _ = upload_batch(other)
+    pred = torch.empty(b.n, dtype=torch.float32, device="cuda")
+    idx = torch.full((w.batch_cap,), -1, dtype=torch.int32, device="cuda")
+    cnt = torch.zeros(1, dtype=torch.int32, device="cuda")
+    # eager reference; the same call also sizes the cached workspaces before capture
+    pr.predict(ids, cu, b.max_seqlen, out_pred=pred)
+    pr.select(pred, arr, w.batch_cap, idx, cnt)
+    torch.cuda.synchronize()
+    ref_pred, ref_idx, ref_cnt = pred.clone(), idx.clone(), cnt.clone()
+    pr.predict(o_ids, o_cu, other.max_seqlen)  # a larger workspace now, before capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g):
+            pr.predict(ids, cu, b.max_seqlen, out_pred=pred)
+            pr.select(pred, arr, w.batch_cap, idx, cnt)
+    torch.cuda.current_stream().wait_stream(side)
+    for rep in range(4):
+        pred.fill_(float("nan"))
+        idx.fill_(-7)
+        cnt.fill_(-7)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(pred.view(torch.int32), ref_pred.view(torch.int32)), rep
+        assert torch.equal(cnt, ref_cnt) and torch.equal(idx, ref_idx), rep
+        # eager work on another batch between replays (it shares the predictor's workspace)
+        p_other, _ = pr.predict(o_ids, o_cu, other.max_seqlen)
+        torch.cuda.synchronize()
+        assert torch.isfinite(p_other).all()
+    st, bits = pr.status()
+    assert st == E.ELIS_OK, (st, bits)
