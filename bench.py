@@ -111,6 +111,8 @@ def _gemm_kernel(bm, bn, wgs, epi, n, f32):
         return f"gemm_sched_kernel<128, 128, 2, 2, 32, {epi}, 64, 2, 2>"
     if (bm, bn) == (64, 128):
         return f"gemm_sched_kernel<64, 128, 2, 2, 32, {epi}, 64, {wgs}, {2 if wgs == 2 else 4}>"
+    if (bm, bn) == (64, 64):
+        return f"gemm_sched_kernel<64, 64, 2, 2, 32, {epi}, 64, {wgs}, {2 if wgs == 4 else 4}>"
     return f"gemm_kernel<128, 64, 2, 2, 16, {epi}>"
 
 
@@ -502,7 +504,8 @@ def gemm_plans(reps=8):
         bias = torch.zeros(n, device=dev)
         res = torch.randn(mmax, n, device=dev) if f32 else None
         o = torch.empty(mmax, n, device=dev, dtype=torch.float32 if f32 else torch.bfloat16)
-        tiles = [t for t in ((256, 256, 1), (128, 128, 2), (64, 128, 2), (64, 128, 1)) if n % t[1] == 0]
+        tiles = [t for t in ((256, 256, 1), (128, 128, 2), (64, 128, 2), (64, 128, 1), (64, 64, 4), (64, 64, 2))
+                 if n % t[1] == 0]
         for m in GEMM_PLAN_MS:
             plans = []
             for t in tiles:
@@ -545,7 +548,7 @@ def summarize_gemm_plans(js, command):
     rows = rec["gemm_plans"]
 
     def tile(p):
-        return f"{p[0]}×{p[1]}" + ("/1" if p[:3] == [64, 128, 1] else "")
+        return f"{p[0]}×{p[1]}/{p[2]}"
 
     def label(p):
         return tile(p) if p[4] == 0 else f"{tile(p)} + {tile(p[4:7])} from row {p[3]:,}"
@@ -553,8 +556,9 @@ def summarize_gemm_plans(js, command):
              "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
              "For each encoder product of BERT-base and XLM-R-large (fp32-out products with the plain residual) "
              "and each token count M, every plan the library can choose from is timed through "
-             "`elis_linear_with_plan`: one launch of 256×256, 128×128, 64×128 (2 per CU) or 64×128/1 (1 per CU, "
-             "4 stages) tiles, or large tiles over the rows that fill whole rounds plus a second launch of another "
+             "`elis_linear_with_plan`: one launch of tiles (written rows×columns/work-groups per CU: 256×256/1, "
+             "128×128/2, 64×128/2, 64×128/1 with 4 stages, 64×64/4, 64×64/2 with 4 stages), or large tiles over "
+             "the rows that fill whole rounds plus a second launch of another "
              "configuration over the rest. `chosen` is `elis_linear_plan`'s pick (the launch-time model); "
              "`fastest` the best measured; the fixed columns are what one configuration alone takes.", "",
              "| shape | chosen / fastest, summed over M | 256×256 alone | 128×128 alone |", "|---|---:|---:|---:|"]

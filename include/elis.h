@@ -307,7 +307,8 @@ int elis_linear_plan(int32_t m, int32_t n, int32_t k, int32_t epilogue, int32_t 
 /*
  * elis_linear with the launch plan given instead of chosen: plan[7] in the
  * layout elis_linear_plan writes. Tiles: 256 x 256 (1 work-group per CU),
- * 128 x 128 (2), 64 x 128 (2 or 1; the latter four-stage), 128 x 64 (2;
+ * 128 x 128 (2), 64 x 128 (2 or 1; the latter four-stage), 64 x 64 (4 or 2;
+ * the latter four-stage), 128 x 64 (2;
  * single launch, and only for n an odd multiple of 64, where it is the only
  * tile); main_bn and rest_bn must divide n, 1 <= m1 <= m, m1 a multiple of
  * main_bm when m1 < m, rest different from main. Every valid plan gives the

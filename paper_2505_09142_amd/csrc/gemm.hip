@@ -15,7 +15,7 @@
 //                      (operand fragments double-buffered in registers, MFMAs of the
 //                      last k-step of a slab issued after the slab barrier) and an
 //                      epilogue staged through LDS for full-line stores; tiles of
-//                      256 x 256, 128 x 128 and 64 x 128.
+//                      256 x 256, 128 x 128, 64 x 128 and 64 x 64.
 //
 // LDS layout. A k-slab row of 64 bf16 is eight 16-byte chunks; the chunk index
 // is XOR-swizzled with the row so the rows one MFMA operand read touches fall on
@@ -614,6 +614,8 @@ hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uin
         case 32: return launch_sched<128, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 33: return launch_sched<64, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         case 34: return launch_sched<64, 128, 2, 2, 32, 64, 1, 4>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 35: return launch_sched<64, 64, 2, 2, 32, 64, 4, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 36: return launch_sched<64, 64, 2, 2, 32, 64, 2, 4>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         default: return hipErrorInvalidValue;
     }
 }
@@ -622,8 +624,8 @@ namespace {
 struct TileShape {
     int cfg, bm, bn, wgs_per_cu;
 };
-constexpr TileShape kTileShapes[] = {{1, 128, 64, 2}, {21, 256, 256, 1}, {32, 128, 128, 2}, {33, 64, 128, 2},
-                                     {34, 64, 128, 1}};
+constexpr TileShape kTileShapes[] = {{1, 128, 64, 2},   {21, 256, 256, 1}, {32, 128, 128, 2}, {33, 64, 128, 2},
+                                     {34, 64, 128, 1},  {35, 64, 64, 4},   {36, 64, 64, 2}};
 }  // namespace
 
 void gemm_config_tile(int cfg, int* bm, int* bn, int* wgs_per_cu) {
@@ -655,28 +657,33 @@ namespace {
 
 // Launch-time model of the scheduled configurations, in microseconds on MI355X (256 CUs),
 // fitted to medians of repeated timings of the BERT-base and XLM-R-large encoder GEMMs
-// (K = 768 .. 4096, one to four rounds of tiles). A launch whose tiles fill R rounds of
-// work-group slots (work-groups per CU x CUs), the last one a fraction f full, takes part(f)
-// for R = 1, else t1 + (R - 2) * beta + part(f) - (t1 - beta) * f; part is piecewise linear
-// through lat (a lone tile, f -> 0), th (f = 1/2) and t1 (f = 1), beta is the cost of one more
-// full round. Each quantity is a + s * K / 64: the slope per 64-deep k-slab is shared by the
-// epilogue kinds, the intercept is per kind (bf16, bf16 + GELU, fp32 + residual). Over every
-// single and split plan of those shapes at 35 sizes (M = 1K .. 92K), timed one by one, the
-// plan it picks is 0.2% slower in total than the fastest one measured.
+// (K = 768 .. 4096, one to four rounds of tiles; all six configurations timed on one box).
+// A launch whose tiles fill R rounds of work-group slots (work-groups per CU x CUs), the last
+// one a fraction f full, takes part(f) for R = 1, else t1 + (R - 2) * beta + part(f)
+// - (t1 - beta) * f; part is piecewise linear through lat (a lone tile, f -> 0), th (f = 1/2)
+// and t1 (f = 1), beta is the cost of one more full round. Each quantity is a + s * K / 64: the slope per 64-deep k-slab is shared by the
+// epilogue kinds, the intercept is per kind (bf16, bf16 + GELU, fp32 + residual). The 64-row
+// tiles are priced only up to the four rounds they were timed on and are not offered past
+// that. Over every single and split plan of those shapes at 35 sizes (M = 1K .. 92K), timed
+// one by one, the plans it picks take 0.4% more time in total than the fastest ones measured.
 struct TileModel {
-    int cfg, bm, bn, occ;
+    int cfg, bm, bn, occ, max_rounds;  // max_rounds: 0 = any; else the fitted range
     float s[4];     // lat, th, t1, beta: slope per k-slab
     float a[3][4];  // intercept per epilogue kind
 };
 constexpr TileModel kTileModels[] = {
-    {21, 256, 256, 1, {1.185f, 1.408f, 1.667f, 1.739f},
-     {{4.81f, 5.68f, 7.52f, 3.94f}, {11.77f, 11.42f, 12.18f, 8.36f}, {10.32f, 14.51f, 22.08f, 28.05f}}},
-    {32, 128, 128, 2, {0.545f, 0.652f, 0.957f, 1.196f},
-     {{3.03f, 4.01f, 4.69f, -0.71f}, {5.15f, 5.64f, 8.13f, 2.30f}, {4.86f, 8.02f, 11.89f, 4.54f}}},
-    {33, 64, 128, 2, {0.341f, 0.581f, 0.609f, 0.578f},
-     {{3.21f, 1.76f, 4.19f, 2.62f}, {3.64f, 2.13f, 4.16f, 3.57f}, {3.97f, 2.82f, 7.97f, 5.24f}}},
-    {34, 64, 128, 1, {0.365f, 0.393f, 0.418f, 0.408f},
-     {{2.80f, 3.13f, 3.41f, 1.62f}, {3.57f, 3.79f, 4.40f, 2.40f}, {3.81f, 4.03f, 4.57f, 3.48f}}},
+    {21, 256, 256, 1, 0, {1.178f, 1.375f, 1.770f, 1.693f},
+     {{6.05f, 5.97f, 5.72f, 4.21f}, {11.77f, 11.79f, 11.15f, 10.12f}, {10.41f, 14.62f, 20.49f, 26.70f}}},
+    {32, 128, 128, 2, 0, {0.535f, 0.614f, 0.991f, 1.073f},
+     {{3.63f, 3.63f, 4.11f, 2.01f}, {5.24f, 6.32f, 7.50f, 4.91f}, {4.94f, 9.43f, 12.78f, 12.17f}}},
+    {33, 64, 128, 2, 4, {0.363f, 0.556f, 0.594f, 0.754f},
+     {{2.94f, 2.37f, 3.95f, 0.42f}, {3.69f, 1.94f, 4.59f, 1.10f}, {3.45f, 3.46f, 8.15f, 3.02f}}},
+    {34, 64, 128, 1, 4, {0.340f, 0.395f, 0.436f, 0.353f},
+     {{3.49f, 2.78f, 2.74f, 2.45f}, {4.11f, 3.68f, 3.67f, 3.50f}, {4.17f, 3.89f, 5.00f, 4.40f}}},
+    {35, 64, 64, 4, 4, {0.227f, 0.481f, 0.757f, 0.844f},
+     {{2.78f, 1.95f, 3.73f, -0.05f}, {3.11f, 1.74f, 4.15f, 0.50f}, {3.24f, 3.77f, 6.41f, 1.22f}}},
+    {36, 64, 64, 2, 4, {0.251f, 0.259f, 0.411f, 0.393f},
+     {{2.47f, 2.85f, 3.10f, 1.40f}, {3.23f, 3.40f, 3.12f, 1.82f}, {2.97f, 4.12f, 4.86f, 2.60f}}},
 };
 constexpr float kSecondLaunchUs = 1.0f;  // dispatch cost of the remainder launch
 
@@ -684,6 +691,9 @@ double model_us(const TileModel& t, int kind, long long m, int n, int k, long lo
     if (m <= 0) return 0.0;
     const long long tiles = (m + t.bm - 1) / t.bm * (n / t.bn), slots = t.occ * cus;
     const long long rounds = (tiles + slots - 1) / slots;
+    // The small tiles were timed over one to four rounds only; past that their cost is not
+    // extrapolated (their many-round behaviour differs) and they are not offered.
+    if (t.max_rounds && rounds > t.max_rounds) return 1e30;
     const double f = static_cast<double>(tiles - (rounds - 1) * slots) / static_cast<double>(slots);
     double v[4];
     for (int q = 0; q < 4; ++q) v[q] = t.a[kind][q] + t.s[q] * (k / 64.0);

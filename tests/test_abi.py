@@ -187,7 +187,7 @@ def test_linear_plan_host_only(lib):
     """The launch plan of a product is host arithmetic: rows split at a whole number of main-tile
     rows, the two launches cover [0, m), tiles of the shapes the library has, and the arguments
     elis_linear rejects are rejected here too."""
-    tiles = {(64, 128), (128, 64), (128, 128), (256, 256)}
+    tiles = {(64, 64), (64, 128), (128, 64), (128, 128), (256, 256)}
     rng = np.random.default_rng(5)
     splits = 0
     for _ in range(400):
@@ -197,11 +197,11 @@ def test_linear_plan_host_only(lib):
         epi = int(rng.integers(0, 3))
         st, (bm, bn, wg, m1, rbm, rbn, rwg) = E.elis_linear_plan(m, n, k, epi)
         assert st == E.ELIS_OK
-        assert (bm, bn) in tiles and n % bn == 0 and wg in (1, 2)
+        assert (bm, bn) in tiles and n % bn == 0 and wg in (1, 2, 4)
         assert 1 <= m1 <= m
         if m1 < m:
             splits += 1
-            assert m1 % bm == 0 and (rbm, rbn) in tiles and n % rbn == 0 and rwg in (1, 2)
+            assert m1 % bm == 0 and (rbm, rbn) in tiles and n % rbn == 0 and rwg in (1, 2, 4)
             assert (rbm, rbn, rwg) != (bm, bn, wg)
             # the first launch fills whole rounds of work-group slots (256 CUs without a GPU): as
             # many whole rows of tiles as fit in the full rounds of a single launch

@@ -345,7 +345,8 @@ def test_linear_split_plans_agree_bitwise():
         # every tile configuration and split forced through elis_linear_with_plan: the same bits
         m = m_max
         forced = [(128, 128, 2, m, 0, 0, 0), (64, 128, 2, m, 0, 0, 0), (64, 128, 1, m, 0, 0, 0),
-                  (128, 128, 2, 8192, 64, 128, 1), (64, 128, 2, 4096, 128, 128, 2)]
+                  (64, 64, 4, m, 0, 0, 0), (64, 64, 2, m, 0, 0, 0),
+                  (128, 128, 2, 8192, 64, 128, 1), (64, 128, 2, 4096, 128, 128, 2), (128, 128, 2, 8192, 64, 64, 4)]
         if n % 256 == 0:
             forced += [(256, 256, 1, m, 0, 0, 0), (256, 256, 1, 4096, 64, 128, 2), (256, 256, 1, 8192, 128, 128, 2)]
         for plan in forced:
