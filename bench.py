@@ -259,20 +259,25 @@ def summarize_mfma(csv_path, bench_json, command):
     import csv
     rec = json.loads([x for x in open(bench_json) if x.startswith("{")][-1])
     vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    durations = collections.defaultdict(dict)  # kernel -> dispatch id -> ns (profiler timestamps)
     with open(csv_path) as f:
         for r in csv.DictReader(f):
             n = re.sub(r"\(.*", "", r["Kernel_Name"].replace("elis::(anonymous namespace)::", "").replace("void ", "")).strip()
             vals[n][r["Counter_Name"]].append(float(r["Counter_Value"]))
+            durations[n][r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    passes = len(durations.get("seqmap_kernel", {}))
     simds, ses = 1024, 32  # MI355X: 256 CUs x 4 SIMDs; 8 XCDs x 4 shader engines
     lines = ["# MFMA busy per kernel: bert_base_b64, rocprofv3 PMC counters", "",
              "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
              "busy = SQ_VALU_MFMA_BUSY_CYCLES / 1024 SIMDs ÷ (SQ_BUSY_CYCLES / 32 shader engines): the fraction of "
              "the kernel's busy cycles in which an average SIMD's matrix core was working. `algorithmic` = "
-             "bench.py's FLOPs ÷ kernel time ÷ 2.5 PFLOP/s from the same run; the ratio algorithmic / busy is "
+             "bench.py's FLOPs per launch ÷ the class's kernel time per launch ÷ 2.5 PFLOP/s, the time taken "
+             f"from the dispatch timestamps of the same run ({passes} forward passes; bench.py's own HIP events "
+             "also time the profiler's per-dispatch counter work under --pmc); the ratio algorithmic / busy is "
              "(clock under load) ÷ 2.4 GHz when the matrix cores run at their full rate while busy.", "",
              "| class | kernels | dispatches | MFMA busy | algorithmic | algorithmic / busy |",
              "|---|---|---:|---:|---:|---:|"]
-    for cls, (knames, _, _) in class_kernels(rec["config"]["workload"].split(":")[0]).items():
+    for cls, (knames, _, per_pass) in class_kernels(rec["config"]["workload"].split(":")[0]).items():
         vs = [vals.get(k) for k in knames]
         if not all(v and v.get("SQ_VALU_MFMA_BUSY_CYCLES") for v in vs):
             continue
@@ -281,7 +286,11 @@ def summarize_mfma(csv_path, bench_json, command):
         bc = sum(sum(v["SQ_BUSY_CYCLES"]) for v in vs)
         busy = mb / simds / (bc / ses)
         k = rec["kernels"].get(cls, {})
-        alg = k.get("tflops", 0.0) / PEAK_BF16_TFLOPS if "tflops" in k else None
+        alg = None
+        if "tflops" in k and passes:
+            flop = k["tflops"] * 1e12 * k["avg_us"] * 1e-6  # per launch, independent of its timing
+            ns = sum(sum(durations[x].values()) for x in knames) / (passes * per_pass)
+            alg = flop / (ns * 1e-9) / 1e12 / PEAK_BF16_TFLOPS
         label = " + ".join(f"`{x}`" for x in knames)
         lines.append(f"| {cls} | {label} | {sum(len(v['SQ_BUSY_CYCLES']) for v in vs)} | {busy:.3f} | "
                      + (f"{alg:.3f} | {alg / busy:.2f} |" if alg is not None and busy > 0 else "- | - |"))
@@ -296,9 +305,10 @@ _ROLES = {"seqmap_kernel": "sequence table", "embed_ln_kernel<3>": "embedding + 
           "head_out_kernel": "head 256->1, affine", COPY_KERNEL: "(torch copies)"}
 
 
-def summarize_trace(stats_csv, command, bench_json):
+def summarize_trace(stats_csv, command, bench_json, plain_json=None):
     """Write the kernel-trace summary from a rocprofv3 --stats kernel_stats.csv and the
-    JSON line bench.py printed in the same run."""
+    JSON line bench.py printed in the same run (plain_json: a line from a run without the
+    profiler on the same box, whose HIP events carry no tracing work)."""
     import csv
     rec = json.loads(open(bench_json).read().strip().splitlines()[-1])
     roles = dict(_ROLES)
@@ -331,6 +341,14 @@ def summarize_trace(stats_csv, command, bench_json):
               + (f"{prof_us:.1f} µs" if prof_us else "n/a") + " (rocprofv3: the class's kernels' total time / its launches); "
               f"{rl['per_launch_flop'] / 1e9:.1f} GFLOP per launch -> {rl['achieved']:.0f} {rl['unit']} = "
               f"{100 * rl['frac']:.1f}% of the {rl['peak']:.0f} {rl['unit']} dense bf16 peak."]
+    if plain_json:
+        p = json.loads([x for x in open(plain_json) if x.startswith("{")][-1])
+        pr = p["roofline"]
+        lines += ["", "Under --kernel-trace the events around a class's launches also take in the tracer's "
+                  "work per dispatch. The same bench.py without the profiler on the same box "
+                  f"(`python bench.py`): {p['ms_per_step']:.3f} ms per step, {p['value']:.0f} seqs/s, "
+                  f"`{pr['kernel']}` {pr['avg_launch_us']:.1f} µs per launch by its HIP events "
+                  f"-> {pr['achieved']:.0f} {pr['unit']} = {100 * pr['frac']:.1f}% of peak."]
     with open(TRACE_PROFILE, "w") as f:
         f.write("\n".join(lines) + "\n")
     print(f"wrote {TRACE_PROFILE}")
@@ -914,8 +932,9 @@ def main():
                     help="time the device-wide select at n = 2^20 .. 2^24 instead of the step")
     ap.add_argument("--summarize-select", nargs=3, metavar=("SWEEP_JSON", "TRACE_CSV", "COMMAND"),
                     help="write the large-n select summary")
-    ap.add_argument("--summarize-trace", nargs=3, metavar=("STATS_CSV", "BENCH_JSON", "COMMAND"),
-                    help="write the kernel-trace summary from a rocprofv3 kernel_stats.csv")
+    ap.add_argument("--summarize-trace", nargs="+", metavar="ARG",
+                    help="write the kernel-trace summary from a rocprofv3 kernel_stats.csv: "
+                         "STATS_CSV BENCH_JSON COMMAND [PLAIN_BENCH_JSON]")
     ap.add_argument("--summarize-mfma", nargs=3, metavar=("PMC_CSV", "BENCH_JSON", "COMMAND"),
                     help="write the MFMA-busy summary from a SQ_VALU_MFMA_BUSY_CYCLES / SQ_BUSY_CYCLES pass")
     ap.add_argument("--pmc-command", action="append", default=[],
@@ -955,7 +974,10 @@ def main():
         summarize_gemm_plans(*args.summarize_gemm_plans)
         return
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace[0], args.summarize_trace[2], args.summarize_trace[1])
+        a = args.summarize_trace  # STATS_CSV BENCH_JSON COMMAND [PLAIN_BENCH_JSON]
+        if len(a) not in (3, 4):
+            ap.error("--summarize-trace takes STATS_CSV BENCH_JSON COMMAND [PLAIN_BENCH_JSON]")
+        summarize_trace(a[0], a[2], a[1], a[3] if len(a) == 4 else None)
         return
     if args.summarize_mfma:
         summarize_mfma(*args.summarize_mfma)
