@@ -277,7 +277,7 @@ int elis_jobs_select_aged(const elis_job_table *t, const int32_t *slots, const f
 
 /* Epilogues of elis_linear. */
 #define ELIS_EPI_BIAS_BF16      0 /* out bf16 = x W^T + b                        */
-#define ELIS_EPI_BIAS_GELU_BF16 1 /* out bf16 = GELU(x W^T + b), exact erf GELU  */
+#define ELIS_EPI_BIAS_GELU_BF16 1 /* out bf16 = GELU(x W^T + b), erf GELU, 1.5e-6 */
 #define ELIS_EPI_BIAS_RES_F32   2 /* out fp32 = x W^T + b + residual             */
 
 /*

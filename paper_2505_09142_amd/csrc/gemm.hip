@@ -72,20 +72,20 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblk) {
 // plain row & 7 form conflicts 4-way on 32-row reads).
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
-// GELU(x) = x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)), with erf from Abramowitz & Stegun 7.1.26:
-// for z >= 0, erfc(z) = (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-z^2) + e(z),
-// t = 1 / (1 + p z), |e(z)| <= 1.5e-7. Since erf is odd, x * Phi(x) = max(x, 0) - |x| * h with
-// h = erfc(|x| / sqrt 2) / 2, so no branch or select on the sign: one reciprocal, one exp2,
-// six FMAs and four multiplies (the 1/2 and 1/sqrt 2 are folded into the constants).
+// GELU(x) = x * Phi(x) = max(x, 0) - a * Phi(-a) with a = |x| (as Phi(-a) = 1 - Phi(a)), so no
+// branch or select on the sign. log2 Phi(-a) is smooth on [0, 5]: a degree-7 polynomial fitted
+// there by weighted least squares (weight a * Phi(-a), the error it makes in GELU) gives Phi(-a)
+// through one exp2. Past a = 5 the clamp leaves less than 5 * Phi(-5) < 1.5e-6 of error. Over
+// all floats the result is within 1.5e-6 absolute and 3e-5 relative (where |GELU| > 1e-3) of
+// x * Phi(x), far below the bf16 rounding of the output: one exp2, eight FMAs, a min and a max
+// (a rational erf approximation needs a reciprocal as well, and measured 5% slower on FFN1).
 __device__ __forceinline__ float gelu_erf(float x) {
-    constexpr float p = 0.3275911f * 0.70710678118654752f;
-    constexpr float a1 = 0.5f * 0.254829592f, a2 = 0.5f * -0.284496736f, a3 = 0.5f * 1.421413741f,
-                    a4 = 0.5f * -1.453152027f, a5 = 0.5f * 1.061405429f;
-    const float ax = fabsf(x);
-    const float t = __builtin_amdgcn_rcpf(fmaf(p, ax, 1.0f));
-    const float poly = t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, a5, a4), a3), a2), a1);
-    const float h = poly * __builtin_amdgcn_exp2f((x * x) * -0.72134752044448170f);  // exp(-x^2 / 2)
-    return fmaf(-ax, h, fmaxf(x, 0.f));
+    constexpr float c0 = -9.999995232e-01f, c1 = -1.151127219e+00f, c2 = -4.590456784e-01f,
+                    c3 = -5.294791982e-02f, c4 = 7.674183231e-03f, c5 = -5.793952732e-04f,
+                    c6 = -1.149886975e-05f, c7 = 4.121166967e-06f;
+    const float a = fminf(fabsf(x), 5.0f);
+    const float q = fmaf(fmaf(fmaf(fmaf(fmaf(fmaf(fmaf(c7, a, c6), a, c5), a, c4), a, c3), a, c2), a, c1), a, c0);
+    return fmaf(-a, __builtin_amdgcn_exp2f(q), fmaxf(x, 0.f));
 }
 
 // One MFMA block of the wave tile: MI x MI outputs (MI = 16: 16x16x32, MI = 32: 32x32x16).
