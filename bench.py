@@ -561,6 +561,112 @@ def gemm_plans(reps=8):
     print(json.dumps({"gemm_plans": out, "cus": cus}), flush=True)
 
 
+VENDOR_GEMM_MS = (2560, 23931, 92000)
+VENDOR_GEMM_PROFILE = os.path.join(ROOT, "profiles", "gemm_vs_hipblaslt.md")
+
+
+def vendor_gemm(reps=20):
+    """The encoder products through elis_linear (the library's own plan and epilogue) next to
+    torch's bf16 linear on the same device (hipBLASLt), for reference: the same product with its
+    bias in bf16 (like for like), and for the GELU and residual products the library's fused
+    epilogue against the vendor product plus torch's separate GELU / residual add."""
+    import torch
+    import torch.nn.functional as F
+
+    from paper_2505_09142_amd import _elis as E
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    g = torch.Generator(device="cpu").manual_seed(0)
+    mmax = max(VENDOR_GEMM_MS)
+
+    def timed(fn):
+        best = None
+        for _ in range(2):  # two passes, the faster kept
+            for _ in range(3):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / reps * 1e3
+            best = us if best is None else min(best, us)
+        return best
+
+    rows = []
+    for name, n, k, epi in GEMM_PLAN_SHAPES:
+        x = (torch.randn(mmax, k, generator=g) * 0.5).to(torch.bfloat16).to(dev)
+        w = (torch.randn(n, k, generator=g) * 0.03).to(torch.bfloat16).to(dev)
+        bias = (torch.randn(n, generator=g) * 0.1).to(dev)
+        bias16 = bias.to(torch.bfloat16)
+        res = torch.randn(mmax, n, device=dev) if epi == 2 else None
+        ob = torch.empty(mmax, n, device=dev, dtype=torch.bfloat16)
+        of = torch.empty(mmax, n, device=dev, dtype=torch.float32) if epi == 2 else None
+        for m in VENDOR_GEMM_MS:
+            xm = x[:m]
+
+            def ours(e):
+                o = of if e == 2 else ob
+                E.check(E.elis_linear(xm.data_ptr(), w.data_ptr(), bias.data_ptr(),
+                                      res.data_ptr() if e == 2 else None, m, n, k, e, o.data_ptr(), stream), name)
+
+            r = {"shape": name, "m": m, "n": n, "k": k, "epi": epi, "flop": 2.0 * m * n * k,
+                 "ours_bias_us": timed(lambda: ours(0)),
+                 "vendor_bias_us": timed(lambda: F.linear(xm, w, bias16))}
+            if epi == 1:
+                r["ours_epi_us"] = timed(lambda: ours(1))
+                r["vendor_epi_us"] = timed(lambda: F.gelu(F.linear(xm, w, bias16)))
+            elif epi == 2:
+                rm = res[:m]
+                r["ours_epi_us"] = timed(lambda: ours(2))
+                r["vendor_epi_us"] = timed(lambda: torch.add(rm, F.linear(xm, w, bias16)))
+            rows.append(r)
+            print(f"{name} m={m}: ours {r['ours_bias_us']:.1f} us, vendor {r['vendor_bias_us']:.1f} us",
+                  file=sys.stderr, flush=True)
+        del x, w, res, ob, of
+    print(json.dumps({"vendor_gemm": rows, "device": torch.cuda.get_device_name(0),
+                      "torch": torch.__version__}), flush=True)
+
+
+def summarize_vendor_gemm(js, command):
+    d = json.loads([x for x in open(js) if x.startswith("{")][-1])
+    rows = d["vendor_gemm"]
+    tf = lambda r, key: r["flop"] / (r[key] * 1e-6) / 1e12
+    lines = ["# Encoder GEMMs: this library vs torch's bf16 linear (hipBLASLt), same device", "",
+             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             f"torch {d['torch']} on {d['device']}. Each product is timed as the best of two passes of 20 "
+             "back-to-back calls (HIP events, inputs resident). `bias` columns: the same product and bias, "
+             "bf16 out (this library: `elis_linear` with the bf16 bias epilogue and its own launch plan; "
+             "vendor: `F.linear`). `fused` columns: the product as the encoder runs it, this library's "
+             "fused epilogue (GELU, or fp32 out plus the residual) against `F.linear` followed by "
+             "torch's `F.gelu` or residual add. TFLOP/s counts 2·M·N·K; % is of the 2500 TFLOP/s dense "
+             "bf16 peak.", "",
+             "| shape | M | N | K | bias: ours µs | vendor µs | ours / vendor speed | ours % peak | "
+             "vendor % peak | fused: ours µs | vendor µs | speed-up |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        fused = (f"{r['ours_epi_us']:.1f} | {r['vendor_epi_us']:.1f} | {r['vendor_epi_us'] / r['ours_epi_us']:.2f}×"
+                 if "ours_epi_us" in r else "- | - | -")
+        lines.append(f"| {r['shape']} | {r['m']:,} | {r['n']} | {r['k']} | {r['ours_bias_us']:.1f} | "
+                     f"{r['vendor_bias_us']:.1f} | {r['vendor_bias_us'] / r['ours_bias_us']:.2f}× | "
+                     f"{100 * tf(r, 'ours_bias_us') / PEAK_BF16_TFLOPS:.1f} | "
+                     f"{100 * tf(r, 'vendor_bias_us') / PEAK_BF16_TFLOPS:.1f} | {fused} |")
+    tot_o = sum(r["ours_bias_us"] for r in rows)
+    tot_v = sum(r["vendor_bias_us"] for r in rows)
+    lines += ["", f"Summed over all rows (bias epilogue): this library {tot_o:,.0f} µs, vendor {tot_v:,.0f} µs "
+              f"({tot_v / tot_o:.2f}×)."]
+    fo = [r for r in rows if "ours_epi_us" in r]
+    if fo:
+        a, b = sum(r["ours_epi_us"] for r in fo), sum(r["vendor_epi_us"] for r in fo)
+        lines.append(f"Fused products (GELU and residual rows): this library {a:,.0f} µs, vendor + torch "
+                     f"{b:,.0f} µs ({b / a:.2f}×).")
+    with open(VENDOR_GEMM_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {VENDOR_GEMM_PROFILE}")
+
+
 def summarize_gemm_plans(js, command):
     rec = json.loads([x for x in open(js) if x.startswith("{")][-1])
     rows = rec["gemm_plans"]
@@ -926,6 +1032,10 @@ def main():
                     help="write the policy-study summary")
     ap.add_argument("--gemm-plans", action="store_true",
                     help="time every GEMM launch plan against the library's choice (encoder products, M = 1K .. 92K)")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="time the encoder GEMMs against torch's bf16 linear (hipBLASLt) on the same device")
+    ap.add_argument("--summarize-vendor-gemm", nargs=2, metavar=("JSON", "COMMAND"),
+                    help="write the GEMM-vs-vendor summary")
     ap.add_argument("--summarize-gemm-plans", nargs=2, metavar=("JSON", "COMMAND"),
                     help="write the GEMM launch-plan summary")
     ap.add_argument("--select-sweep", action="store_true",
@@ -969,6 +1079,12 @@ def main():
         return
     if args.gemm_plans:
         gemm_plans()
+        return
+    if args.vendor_gemm:
+        vendor_gemm()
+        return
+    if args.summarize_vendor_gemm:
+        summarize_vendor_gemm(*args.summarize_vendor_gemm)
         return
     if args.summarize_gemm_plans:
         summarize_gemm_plans(*args.summarize_gemm_plans)
