@@ -665,7 +665,8 @@ namespace {
 // epilogue kinds, the intercept is per kind (bf16, bf16 + GELU, fp32 + residual). The 64-row
 // tiles are priced only up to the four rounds they were timed on and are not offered past
 // that. Over every single and split plan of those shapes at 35 sizes (M = 1K .. 92K), timed
-// one by one, the plans it picks take 0.4% more time in total than the fastest ones measured.
+// one by one, the plans it picks take 0.25-0.4% more time in total than the fastest ones
+// measured (two boxes).
 struct TileModel {
     int cfg, bm, bn, occ, max_rounds;  // max_rounds: 0 = any; else the fitted range
     float s[4];     // lat, th, t1, beta: slope per k-slab
