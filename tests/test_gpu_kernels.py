@@ -201,6 +201,29 @@ def test_linear(m, n, k, epi):
         assert np.all(np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 1.2 * acc_tol), np.abs(got - ref).max()
 
 
+def test_gelu_epilogue_sweep():
+    """The GELU epilogue over a dense sweep of pre-activations, tails and clamp included: with
+    x = 0 and W = 0 the product is exactly the bias, so each output is bf16(GELU(bias[n]))."""
+    m, n, k = 3, 8192, 64
+    special = np.array([0.0, -0.0, 5.0, -5.0, 4.9999, -4.9999, 5.0001, -5.0001, 20.0, -20.0, 100.0, -100.0,
+                        1e4, -1e4, 1e-30, -1e-30, 1e-3, -1e-3, 0.5, -0.5], np.float32)
+    sweep = np.linspace(-8.0, 8.0, n - special.size, dtype=np.float32)
+    bias = np.concatenate([sweep, special]).astype(np.float32)
+    note(f"gelu epilogue sweep m={m} n={n} k={k}")
+    d_x = dev(np.zeros((m, k), np.uint16))
+    d_w = dev(np.zeros((n, k), np.uint16))
+    d_bias = dev(bias)
+    out = torch.empty((m, n), dtype=torch.int16, device="cuda")
+    ok(E.elis_linear(d_x.data_ptr(), d_w.data_ptr(), d_bias.data_ptr(), None, m, n, k, E.ELIS_EPI_BIAS_GELU_BF16,
+                     out.data_ptr(), stream()))
+    torch.cuda.synchronize()
+    got = bf16_to_f64(host_u16(out))
+    ref = oracle.gelu(bias.astype(np.float64))
+    err = np.abs(got - ref[None, :])
+    assert np.all(err <= 2.0 ** -8 * np.abs(ref)[None, :] + 2e-6), (err.max(), bias[np.argmax(err.max(axis=0))])
+    assert np.array_equal(got[0], got[1]) and np.array_equal(got[0], got[2])
+
+
 # ------------------------------------------------------------------------------ attention
 
 ATT_LENS = [
