@@ -214,7 +214,7 @@ def summarize_pmc(fetch_csv, write_csv, copy_mib, workload, commands):
     mandatory["attention"] = ((L - 1) * (qkv_b + T * d * 2) + att_tail) / L
     passes = len(fetch.get("seqmap_kernel", []))
     lines = [f"# HBM traffic per launch: {workload} (T = {T:,}), rocprofv3 PMC byte counters", "",
-             "Two passes over the same bench command, one counter each (GPU box, repo root as working tree):", ""]
+             "Two passes over the same bench command, one counter each (MI355X, repo root as working tree):", ""]
     lines += [f"    {c}" for c in commands]
     lines += ["", f"Scale: before its steps each pass runs a plain device-to-device copy of {copy_mib} MiB "
               f"three times (`{COPY_KERNEL}`). Counter readings of those copies: FETCH_SIZE "
@@ -268,7 +268,7 @@ def summarize_mfma(csv_path, bench_json, command):
     passes = len(durations.get("seqmap_kernel", {}))
     simds, ses = 1024, 32  # MI355X: 256 CUs x 4 SIMDs; 8 XCDs x 4 shader engines
     lines = ["# MFMA busy per kernel: bert_base_b64, rocprofv3 PMC counters", "",
-             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "Command (MI355X, repo root as working tree):", "", f"    {command}", "",
              "busy = SQ_VALU_MFMA_BUSY_CYCLES / 1024 SIMDs ÷ (SQ_BUSY_CYCLES / 32 shader engines): the fraction of "
              "the kernel's busy cycles in which an average SIMD's matrix core was working. `algorithmic` = "
              "bench.py's FLOPs per launch ÷ the class's kernel time per launch ÷ 2.5 PFLOP/s, the time taken "
@@ -330,7 +330,7 @@ def summarize_trace(stats_csv, command, bench_json, plain_json=None):
     cfg = rec["config"]
     steps, warm = rec["steps"], rec["warmup"]
     lines = [f"# Kernel trace: {cfg['workload'].split(':')[0]} (T = {cfg['total_tokens']:,}), predict + select", "",
-             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "Command (MI355X, repo root as working tree):", "", f"    {command}", "",
              f"{warm + 2 * steps} forward passes were traced ({warm} warm-up + {steps} per-class-timed + {steps} "
              "timed steps). Table from the `kernel_stats.csv` of that run.", "",
              "| kernel | class | calls | total µs | avg µs | % of GPU time |", "|---|---|---:|---:|---:|---:|"]
@@ -371,7 +371,7 @@ def summarize_select(sweep_json, trace_csv, command):
     calls = [tr[i:i + nk] for i in range(0, len(tr), nk)]
     per_cfg = len(calls) // len(rows)
     lines = ["# ISRTF select above 8192 jobs: device-wide radix selection, n = 2^20 .. 2^24", "",
-             "Commands (GPU box, repo root as working tree):", "",
+             "Commands (MI355X, repo root as working tree):", "",
              "    python bench.py --select-sweep", f"    {command}", "",
              "Predictions 250 + 100 * N(0, 0.55^2) (the predictor's output scale), arrivals a random "
              "permutation. `mandatory` = 12 n bytes in (pred + arrival) + 4 k out; HBM fraction = "
@@ -404,7 +404,7 @@ def summarize_rounds(rounds_json):
     """Write the ISRTF round-latency summary from bench.py --isrtf-rounds' line."""
     rec = json.loads(open(rounds_json).read().strip().splitlines()[-1])["isrtf_rounds"]
     lines = [f"# ISRTF scheduling rounds: device-resident job table vs host packing", "",
-             "Command (GPU box, repo root as working tree):", "", "    python bench.py --isrtf-rounds", "",
+             "Command (MI355X, repo root as working tree):", "", "    python bench.py --isrtf-rounds", "",
              f"{rec['workload']}; the whole stream, every round timed on the host from the start of the "
              "re-score to the chosen jobs on the host. Both drivers produce the same schedule "
              f"(`same_schedule`: {rec['same_schedule']}).", "",
@@ -635,7 +635,7 @@ def summarize_vendor_gemm(js, command):
     rows = d["vendor_gemm"]
     tf = lambda r, key: r["flop"] / (r[key] * 1e-6) / 1e12
     lines = ["# Encoder GEMMs: this library vs torch's bf16 linear (hipBLASLt), same device", "",
-             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "Command (MI355X, repo root as working tree):", "", f"    {command}", "",
              f"torch {d['torch']} on {d['device']}. Each product is timed as the best of two passes of 20 "
              "back-to-back calls (HIP events, inputs resident). `bias` columns: the same product and bias, "
              "bf16 out (this library: `elis_linear` with the bf16 bias epilogue and its own launch plan; "
@@ -677,7 +677,7 @@ def summarize_gemm_plans(js, command):
     def label(p):
         return tile(p) if p[4] == 0 else f"{tile(p)} + {tile(p[4:7])} from row {p[3]:,}"
     lines = ["# GEMM launch plans: every plan timed vs the one the library picks", "",
-             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "Command (MI355X, repo root as working tree):", "", f"    {command}", "",
              "For each encoder product of BERT-base and XLM-R-large (fp32-out products with the plain residual) "
              "and each token count M, every plan the library can choose from is timed through "
              "`elis_linear_with_plan`: one launch of tiles (written rows×columns/work-groups per CU: 256×256/1, "
@@ -835,7 +835,7 @@ def rounds_b256():
 def summarize_rounds100(js, command):
     rec = json.loads(open(js).read().strip().splitlines()[-1])["rounds_b256"]
     lines = ["# 100 scheduling rounds at 256 in-flight sequences (BERT-base-shaped predictor)", "",
-             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "Command (MI355X, repo root as working tree):", "", f"    {command}", "",
              f"{rec['workload']}. Every round appends each sequence's new token to the device job table, packs "
              "all 256 inputs on the device (first token plus the most recent 511 past 512), re-predicts every one "
              "and selects 128; one host synchronisation per round (the chosen slots).", "",
@@ -855,7 +855,7 @@ WORKLOADS_PROFILE = os.path.join(ROOT, "profiles", "workloads_summary.md")
 def summarize_workloads(paths, command):
     """One table over bench.py lines of several --workload runs."""
     lines = ["# Predict + select per workload (one MI355X)", "",
-             "Command (GPU box, repo root as working tree), once per workload:", "", f"    {command}", "",
+             "Command (MI355X, repo root as working tree), once per workload:", "", f"    {command}", "",
              "One step = elis_predict_remaining + elis_isrtf_select on a batch resident in HBM; GEMM and attention "
              "MFMA utilisation = algorithmic FLOPs / per-class kernel time / 2.5 PFLOP/s (HIP events around each "
              "launch); the roofline column is bench.py's dominant kernel class.", "",
@@ -956,7 +956,7 @@ def summarize_policy(study_json, command):
     caps = sorted({k[1] for k in mean})
     rpss = sorted({k[2] for k in mean})
     lines = ["# Scheduler policy study (synthetic analogue of Fig. 5 and 6)", "",
-             "Command (GPU box, repo root as working tree):", "", f"    {command}", "",
+             "Command (MI355X, repo root as working tree):", "", f"    {command}", "",
              f"{rec['requests']} synthetic requests per run (prompt lognormal(200, 0.8), response lognormal(250, 1.0) "
              f"capped at 2048), Gamma(shape {rec['gamma_shape']}) request intervals at k x batch / (mean response "
              f"length x {rec['step_cost_s'] * 1e3:g} ms per decode step) requests/s, {rec['window']}-token windows, "
