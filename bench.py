@@ -299,6 +299,58 @@ def summarize_mfma(csv_path, bench_json, command):
     print(f"wrote {MFMA_PROFILE}")
 
 
+ISSUE_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_issue_counters.md")
+ISSUE_COUNTERS = ("SQ_BUSY_CYCLES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_VALU_TRANS_F32",
+                  "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_ACTIVE_INST_VALU")
+
+
+def summarize_issue(csv_path, command):
+    """Instruction mix and LDS bank conflicts per kernel class from one rocprofv3 --pmc pass
+    with ISSUE_COUNTERS (summed over every dispatch of the class's kernels)."""
+    import collections
+    import csv
+    vals = collections.defaultdict(lambda: collections.defaultdict(float))
+    disp = collections.defaultdict(set)
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            n = re.sub(r"\(.*", "", r["Kernel_Name"].replace("elis::(anonymous namespace)::", "").replace("void ", "")).strip()
+            vals[n][r["Counter_Name"]] += float(r["Counter_Value"])
+            disp[n].add(r["Dispatch_Id"])
+    simds, ses = 1024, 32  # MI355X: 256 CUs x 4 SIMDs; 8 XCDs x 4 shader engines
+    lines = ["# Instruction mix and LDS bank conflicts per kernel class: bert_base_b64, rocprofv3 PMC counters", "",
+             "Command (MI355X, repo root as working tree):", "", f"    {command}", "",
+             "Counters summed over every dispatch of a class's kernels. `VALU / MFMA` = (SQ_INSTS_VALU − "
+             "SQ_INSTS_MFMA) / SQ_INSTS_MFMA (SQ_INSTS_VALU counts the matrix instructions too); `trans / MFMA` "
+             "= SQ_INSTS_VALU_TRANS_F32 / SQ_INSTS_MFMA. `VALU issue` = 4 cycles per non-matrix VALU "
+             "instruction (a wave64 instruction on a 16-lane SIMD) ÷ 1024 SIMDs ÷ (SQ_BUSY_CYCLES / 32 shader "
+             "engines): the fraction of the kernel's cycles an average SIMD's vector ALU spent issuing, "
+             "transcendentals counted at one pass. `LDS conflicts` = SQ_LDS_BANK_CONFLICT / (SQ_LDS_IDX_ACTIVE − "
+             "SQ_LDS_BANK_CONFLICT): bank-conflict stall cycles per active LDS cycle.", "",
+             "| class | dispatches | VALU / MFMA | trans / MFMA | VALU issue | LDS conflicts |",
+             "|---|---:|---:|---:|---:|---:|"]
+    rec_cls = class_kernels("bert_base_b64")
+    for cls, (knames, _, _) in rec_cls.items():
+        vs = [vals.get(k) for k in knames]
+        if not all(vs):
+            continue
+        tot = collections.defaultdict(float)
+        for v in vs:
+            for c, x in v.items():
+                tot[c] += x
+        mf = tot["SQ_INSTS_MFMA"]
+        valu = tot["SQ_INSTS_VALU"] - mf
+        cyc = tot["SQ_BUSY_CYCLES"] / ses
+        issue = 4.0 * valu / simds / cyc if cyc else 0.0
+        lds = tot["SQ_LDS_IDX_ACTIVE"] - tot["SQ_LDS_BANK_CONFLICT"]
+        conf = tot["SQ_LDS_BANK_CONFLICT"] / lds if lds > 0 else 0.0
+        lines.append(f"| {cls} | {sum(len(disp[k]) for k in knames)} | "
+                     + (f"{valu / mf:.2f} | {tot['SQ_INSTS_VALU_TRANS_F32'] / mf:.2f}" if mf else "- | -")
+                     + f" | {issue:.2f} | {conf:.3f} |")
+    with open(ISSUE_PROFILE, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"wrote {ISSUE_PROFILE}")
+
+
 TRACE_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_kernel_trace.md")
 _ROLES = {"seqmap_kernel": "sequence table", "embed_ln_kernel<3>": "embedding + LN",
           "select_rank_kernel": "ISRTF select", "head_hidden_kernel": "head 768->256 + ReLU",
@@ -1045,6 +1097,8 @@ def main():
     ap.add_argument("--summarize-trace", nargs="+", metavar="ARG",
                     help="write the kernel-trace summary from a rocprofv3 kernel_stats.csv: "
                          "STATS_CSV BENCH_JSON COMMAND [PLAIN_BENCH_JSON]")
+    ap.add_argument("--summarize-issue", nargs=2, metavar=("PMC_CSV", "COMMAND"),
+                    help="write the instruction-mix / LDS-conflict summary from a --pmc pass of ISSUE_COUNTERS")
     ap.add_argument("--summarize-mfma", nargs=3, metavar=("PMC_CSV", "BENCH_JSON", "COMMAND"),
                     help="write the MFMA-busy summary from a SQ_VALU_MFMA_BUSY_CYCLES / SQ_BUSY_CYCLES pass")
     ap.add_argument("--pmc-command", action="append", default=[],
@@ -1094,6 +1148,9 @@ def main():
         if len(a) not in (3, 4):
             ap.error("--summarize-trace takes STATS_CSV BENCH_JSON COMMAND [PLAIN_BENCH_JSON]")
         summarize_trace(a[0], a[2], a[1], a[3] if len(a) == 4 else None)
+        return
+    if args.summarize_issue:
+        summarize_issue(*args.summarize_issue)
         return
     if args.summarize_mfma:
         summarize_mfma(*args.summarize_mfma)
