@@ -67,8 +67,15 @@ __global__ __launch_bounds__(kThreads) void select_rank_kernel(const float* __re
     if (i < n) {
         const uint32_t ki = sk[i];
         const int64_t ai = sa[i];
+        // rank = number of jobs ordered before job i (key, then arrival, then index), counted
+        // without branches so the LDS reads of consecutive j overlap
         int rank = 0;
-        for (int j = 0; j < n; ++j) rank += key_less(sk[j], sa[j], j, ki, ai, i) ? 1 : 0;
+#pragma unroll 8
+        for (int j = 0; j < n; ++j) {
+            const uint32_t kj = sk[j];
+            const int64_t aj = sa[j];
+            rank += static_cast<int>((kj < ki) | ((kj == ki) & ((aj < ai) | ((aj == ai) & (j < i)))));
+        }
         if (rank < k) out_idx[rank] = i;
     }
     if (i == 0) {
@@ -641,8 +648,9 @@ hipError_t launch_select(const float* pred, const int64_t* arrival, int n, int k
     if (n < 1 || n > kLargeMaxN || k < 0) return hipErrorInvalidValue;
     uint32_t* status = static_cast<uint32_t*>(workspace);
     if (n <= kRankMaxN) {
-        ELIS_TRY(launch_kernel(select_rank_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, n, k, out_idx, out_count,
-                           status));
+        const int threads = (n + kWave - 1) / kWave * kWave;  // one thread per job, whole waves
+        ELIS_TRY(launch_kernel(select_rank_kernel, dim3(1), dim3(threads), 0, st, pred, arrival, n, k, out_idx, out_count,
+                               status));
         return hipSuccess;
     }
     if (n <= kSortMaxN) {
