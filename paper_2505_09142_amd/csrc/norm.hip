@@ -84,9 +84,17 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void embed_ln_kernel(
     LnOut out, uint32_t* __restrict__ status) {
     const int lane = threadIdx.x & (kWave - 1);
     const int t = blockIdx.x * kRowsPerBlock + (threadIdx.x / kWave);
+    // Up to 255 sequences, the segment search runs over a copy of cu in LDS (one load per
+    // thread, then LDS latency per search step instead of a dependent global load).
+    __shared__ int32_t cu_s[kRowsPerBlock * kWave];
+    const bool staged = n < kRowsPerBlock * kWave;  // n + 1 entries fit; uniform
+    if (staged) {
+        for (int i = threadIdx.x; i <= n; i += kRowsPerBlock * kWave) cu_s[i] = cu[i];
+        __syncthreads();
+    }
     if (t >= total) return;
-    const int s = find_segment(cu, n, t);
-    int p = t - cu[s];
+    const int s = staged ? find_segment(cu_s, n, t) : find_segment(cu, n, t);
+    int p = t - (staged ? cu_s[s] : cu[s]);
     p = p < 0 ? 0 : (p >= max_pos ? max_pos - 1 : p);
     int id = ids[t];
     if (id < 0 || id >= vocab) {
