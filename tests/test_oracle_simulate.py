@@ -211,3 +211,109 @@ def test_aging_zero_equals_plain_select():
                  aging=0.0, prefill_cost=0.0)
     assert [r.selected for r in a.rounds] == [r.selected for r in b.rounds]
     assert np.array_equal(a.finish_t, b.finish_t)
+
+
+# ----------------------------------------------------------------------------- window end and re-scoring rules
+
+def test_first_finish_window_end_hand_example():
+    """end_rule "first" (the alternative reading of the window end, Sec. 4.1): the window ends when
+    the first selected job stops. Three jobs at t = 0 with 4, 15 and 6 response tokens, FCFS keys,
+    two slots, windows of 10 tokens at 0.01 s per step. Worked by hand:
+      t=0     A, B run; A has 4 left, B 10 of its window -> the window lasts 4 steps:
+              A finishes at 0.04, B is credited 4 tokens (not its 10)
+      t=0.04  B (11 left), C (6 left) run          -> 6 steps: C finishes at 0.10, B at 10 tokens
+      t=0.10  B alone, 5 left                      -> finishes at 0.15
+    With end_rule "all" the first window lasts 10 steps (B reaches 10 tokens at 0.10); then B and C
+    run together, B finishing at 0.15 and C at 0.16.
+    """
+    prompts, responses = _jobs([4, 15, 6], 12)
+    kw = dict(window=10, step_cost=0.01, batch_cap=2, max_pos=64, policy="fcfs")
+    first = simulate(np.zeros(3), prompts, responses, end_rule="first", **kw)
+    assert [rr.selected for rr in first.rounds] == [[0, 1], [1, 2], [1]]
+    assert [rr.window_steps for rr in first.rounds] == [4, 6, 5]
+    np.testing.assert_allclose([rr.t for rr in first.rounds], [0.0, 0.04, 0.10], atol=1e-12)
+    np.testing.assert_allclose(first.finish_t, [0.04, 0.15, 0.10], atol=1e-12)
+    assert first.generated.tolist() == [4, 15, 6]
+    every = simulate(np.zeros(3), prompts, responses, end_rule="all", **kw)
+    assert [rr.selected for rr in every.rounds] == [[0, 1], [1, 2]]
+    assert [rr.window_steps for rr in every.rounds] == [10, 6]
+    np.testing.assert_allclose(every.finish_t, [0.04, 0.15, 0.16], atol=1e-12)
+
+
+def test_first_finish_conservation():
+    rng = np.random.default_rng(21)
+    lengths = rng.integers(1, 90, size=30)
+    prompts, responses = _jobs(lengths, 13)
+    arrival = np.sort(rng.uniform(0, 1.0, size=30))
+    res = simulate(arrival, prompts, responses, window=25, step_cost=0.01, batch_cap=4, max_pos=64,
+                   predict_fn=_true_remaining(responses), end_rule="first")
+    assert np.array_equal(res.generated, lengths)
+    for rr in res.rounds:
+        # the window is the shortest of the chosen jobs' budgets min(K, tokens left)
+        assert 1 <= rr.window_steps <= 25
+    assert np.all(res.jct >= lengths * 0.01 - 1e-12)
+
+
+def _counting_predictor(base, drop):
+    """A predictor whose key for job j falls by drop[j] each time j is scored: its output depends on
+    how often a job was re-scored, so re-scoring rules become visible in the trajectory."""
+    calls = {}
+
+    def fn(ids, inputs, g):
+        out = []
+        for j in ids:
+            c = calls.get(j, 0)
+            calls[j] = c + 1
+            out.append(float(base[j] - drop[j] * c))
+        return out
+    return fn
+
+
+def test_rescore_all_rekeys_every_candidate_hand_example():
+    """rescore "all" (reading of cfg5's re-score-all) gives every admitted unfinished job a fresh key
+    each round; "pool" (Alg. 1) only the new arrivals and the jobs that ran. Two jobs of 20 tokens at
+    t = 0, one slot, windows of 10; a predictor whose key for A is 50 - 30 c and for B 60 - 50 c after
+    c earlier scorings. Worked by hand:
+      pool: t=0 A 50, B 60 -> A;  A re-scored 20, B keeps 60 -> A (finishes 0.2);  B 60 -> B;  B 10 -> B
+      all:  t=0 A 50, B 60 -> A;  A 20, B 10 -> B;  A -10, B -40 -> B (finishes 0.3);  A -40 -> A
+    """
+    prompts, responses = _jobs([20, 20], 14)
+    kw = dict(window=10, step_cost=0.01, batch_cap=1, max_pos=64)
+    pool = simulate(np.zeros(2), prompts, responses, predict_fn=_counting_predictor([50, 60], [30, 50]),
+                    rescore="pool", **kw)
+    assert [rr.selected for rr in pool.rounds] == [[0], [0], [1], [1]]
+    assert [rr.rescored for rr in pool.rounds] == [[0, 1], [0], [], [1]]
+    np.testing.assert_allclose(pool.finish_t, [0.2, 0.4], atol=1e-12)
+    every = simulate(np.zeros(2), prompts, responses, predict_fn=_counting_predictor([50, 60], [30, 50]),
+                     rescore="all", **kw)
+    assert [rr.selected for rr in every.rounds] == [[0], [1], [1], [0]]
+    assert [rr.rescored for rr in every.rounds] == [[0, 1], [0, 1], [0, 1], [0]]
+    np.testing.assert_allclose([rr.pred.tolist() for rr in every.rounds[:3]], [[50, 60], [20, 10], [-10, -40]])
+    np.testing.assert_allclose(every.finish_t, [0.4, 0.3], atol=1e-12)
+    for rr in every.rounds:
+        assert rr.rescored == rr.candidates
+
+
+@pytest.mark.parametrize("end_rule", ["all", "first"])
+def test_rescore_all_equals_pool_for_a_deterministic_predictor(end_rule):
+    """A predictor that is a function of the job's input alone gives an unchanged job the key it
+    already has, so re-scoring every job reproduces the Job-Pool trajectory exactly (reading 15)."""
+    rng = np.random.default_rng(31)
+    lengths = rng.integers(1, 200, size=60)
+    prompts, responses = _jobs(lengths, 15)
+    arrival = np.sort(rng.uniform(0, 2.0, size=60))
+
+    def fn(ids, inputs, g):
+        # depends on the input tokens only (length and content)
+        return [float((len(x) * 7919 + int(np.sum(x.astype(np.int64) * np.arange(1, len(x) + 1)))) % 997)
+                for x in inputs]
+
+    kw = dict(window=20, step_cost=0.01, batch_cap=3, max_pos=32, predict_fn=fn, end_rule=end_rule)
+    pool = simulate(arrival, prompts, responses, rescore="pool", **kw)
+    every = simulate(arrival, prompts, responses, rescore="all", **kw)
+    assert len(pool.rounds) == len(every.rounds)
+    for a, b in zip(pool.rounds, every.rounds):
+        assert a.t == b.t and a.selected == b.selected and a.window_steps == b.window_steps
+        assert np.array_equal(a.keys, b.keys)
+        assert set(a.rescored) <= set(b.rescored) and b.rescored == b.candidates
+    assert np.array_equal(pool.finish_t, every.finish_t)
