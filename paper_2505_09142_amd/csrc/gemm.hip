@@ -316,12 +316,13 @@ __device__ __forceinline__ void interleave_step() {
     }
 }
 
-template <int BM, int BN, int WM, int WN, int MI, int EPI, int BK = 64, int OCC = 1, int S = 2>
+template <int BM, int BN, int WM, int WN, int MI, int EPI, int OCC = 1, int S = 2>
 __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void gemm_sched_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, const float* __restrict__ bias,
     Residual res, void* __restrict__ out, int M, int N, int K, int group_m) {
     typedef Mfma<MI> MF;
     typedef typename MF::acc_t acc_t;
+    constexpr int BK = kBK;              // k-slab depth: 64 (eight 16-byte chunks per row)
     constexpr int NW = WM * WN;
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / MI, FN = TN / MI;
@@ -329,7 +330,6 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(O
     constexpr int GROUPS = kWave / MI;     // lane groups along k
     constexpr int CPR = BK / 8;            // 16-byte chunks per slab row
     constexpr int RPI = kWave / CPR;       // slab rows covered by one wave-wide 16-byte load
-    constexpr int SWS = BK == 64 ? 1 : 2;  // swizzle: chunk ^ ((row >> SWS) & (CPR - 1))
     constexpr int LA = BM / RPI / NW, LB = BN / RPI / NW;  // direct loads per wave per stage
     static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "rows must split over the waves");
     constexpr int STAGE = (BM + BN) * BK;
@@ -346,7 +346,7 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(O
 
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const int wm = wid / WN, wn = wid % WN;
-    auto sw = [](int row) { return (row >> SWS) & (CPR - 1); };
+    auto sw = [](int row) { return (row >> 1) & (CPR - 1); };
 
     const uint16_t* ga[LA];
     const uint16_t* gb[LB];
@@ -541,29 +541,29 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(O
     }
 }
 
-template <int BM, int BN, int WM, int WN, int MI, int BK = 64, int OCC = 1, int S = 2>
+template <int BM, int BN, int WM, int WN, int MI, int OCC = 1, int S = 2>
 hipError_t launch_sched(const uint16_t* x, const uint16_t* w, const float* bias, Residual res, int m, int n,
                         int k, int epi, void* out, hipStream_t st, int group_m) {
     const dim3 grid(((m + BM - 1) / BM) * (n / BN)), block(WM * WN * kWave);
     switch (epi) {
         case ELIS_EPI_BIAS_BF16:
-            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16, BK, OCC, S>), grid, block, 0, st, x, w, bias,
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_BF16, OCC, S>), grid, block, 0, st, x, w, bias,
                                res, out, m, n, k, group_m));
             break;
         case ELIS_EPI_BIAS_GELU_BF16:
-            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16, BK, OCC, S>), grid, block, 0, st, x, w,
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_GELU_BF16, OCC, S>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m));
             break;
         case ELIS_EPI_BIAS_RES_F32:
-            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, BK, OCC, S>), grid, block, 0, st, x, w,
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, ELIS_EPI_BIAS_RES_F32, OCC, S>), grid, block, 0, st, x, w,
                                bias, res, out, m, n, k, group_m));
             break;
         case kEpiResLn:
-            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLn, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLn, OCC, S>), grid, block, 0, st, x, w, bias, res,
                                out, m, n, k, group_m));
             break;
         case kEpiResLnFfn2:
-            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2, BK, OCC, S>), grid, block, 0, st, x, w, bias, res,
+            ELIS_TRY(launch_kernel((gemm_sched_kernel<BM, BN, WM, WN, MI, kEpiResLnFfn2, OCC, S>), grid, block, 0, st, x, w, bias, res,
                                out, m, n, k, group_m));
             break;
         default:
@@ -611,11 +611,11 @@ hipError_t launch_gemm_config(int cfg, int group_m, const uint16_t* x, const uin
     switch (cfg) {
         case 1: return launch_tile<128, 64, 2, 2, 16>(x, w, bias, res, m, n, k, epi, out, st);
         case 21: return launch_sched<256, 256, 2, 4, 32>(x, w, bias, res, m, n, k, epi, out, st, group_m);
-        case 32: return launch_sched<128, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
-        case 33: return launch_sched<64, 128, 2, 2, 32, 64, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
-        case 34: return launch_sched<64, 128, 2, 2, 32, 64, 1, 4>(x, w, bias, res, m, n, k, epi, out, st, group_m);
-        case 35: return launch_sched<64, 64, 2, 2, 32, 64, 4, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
-        case 36: return launch_sched<64, 64, 2, 2, 32, 64, 2, 4>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 32: return launch_sched<128, 128, 2, 2, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 33: return launch_sched<64, 128, 2, 2, 32, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 34: return launch_sched<64, 128, 2, 2, 32, 1, 4>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 35: return launch_sched<64, 64, 2, 2, 32, 4, 2>(x, w, bias, res, m, n, k, epi, out, st, group_m);
+        case 36: return launch_sched<64, 64, 2, 2, 32, 2, 4>(x, w, bias, res, m, n, k, epi, out, st, group_m);
         default: return hipErrorInvalidValue;
     }
 }
