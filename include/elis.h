@@ -345,6 +345,26 @@ int elis_attention(const uint16_t *qkv, const int32_t *cu_seqlens, int32_t n_seq
 int elis_layernorm(const float *x, const float *g, const float *b, int32_t rows, int32_t d,
                    float eps, float *out_f32, uint16_t *out_bf16, void *stream);
 
+/* Bytes of workspace elis_pool_head needs (0 if the arguments are invalid). */
+size_t elis_pool_head_workspace_bytes(const elis_config *cfg, int32_t n_seqs, int32_t max_seqlen);
+
+/*
+ * Pooling and regression head alone (the last two steps of
+ * elis_predict_remaining): CLS pooling takes each sequence's first row
+ * (Sec. 3.2), mean pooling averages all of its rows (Sec. 4.2); then the
+ * head's head_layers fully connected layers (Sec. 3.2, Sec. 4.2) and the map
+ * to tokens, out_pred[s] = out_shift + out_scale * head(pool(H_s)).
+ *  w           only cfg and the head_* fields are read (the encoder pointers may be NULL).
+ *  hidden      fp32 [total_tokens, d_model] final hidden states, packed as cu_seqlens says.
+ *  cu_seqlens, n_seqs, total_tokens, max_seqlen: as for elis_predict_remaining (content
+ *              errors set bits readable with elis_read_status(workspace)).
+ *  out_pred    fp32 [n_seqs].
+ *  workspace   >= elis_pool_head_workspace_bytes(...) bytes, 256-byte aligned.
+ */
+int elis_pool_head(const elis_weights *w, const float *hidden, const int32_t *cu_seqlens, int32_t n_seqs,
+                   int32_t total_tokens, int32_t max_seqlen, float *out_pred, void *workspace, size_t ws_bytes,
+                   void *stream);
+
 /* ------------------------------------------------------------------ timing (opt-in)
  * When a class is enabled, each timed launch of it enqueues its kernels with
  * a start/stop HIP event pair attached to each dispatch (hipExtLaunchKernel),

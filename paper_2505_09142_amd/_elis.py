@@ -98,6 +98,9 @@ SIGNATURES = {
                                c_size_t, c_void_p]),
     "elis_layernorm": (c_int, [c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_float, c_void_p, c_void_p,
                                c_void_p]),
+    "elis_pool_head_workspace_bytes": (c_size_t, [POINTER(elis_config), c_int32, c_int32]),
+    "elis_pool_head": (c_int, [POINTER(elis_weights), c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p,
+                               c_void_p, c_size_t, c_void_p]),
     "elis_jobs_table_bytes": (c_size_t, [c_int32, c_int32]),
     "elis_jobs_init": (c_int, [POINTER(elis_job_table), c_void_p]),
     "elis_jobs_start": (c_int, [POINTER(elis_job_table), c_void_p, c_void_p, c_int32, c_void_p]),
@@ -209,6 +212,16 @@ def elis_attention(qkv: int, cu_seqlens: int, n_seqs: int, total_tokens: int, ma
 def elis_layernorm(x: int, g: int, b: int, rows: int, d: int, eps: float, out_f32: int | None,
                    out_bf16: int | None, stream: int | None) -> int:
     return lib().elis_layernorm(x, g, b, rows, d, eps, out_f32, out_bf16, stream)
+
+
+def elis_pool_head_workspace_bytes(cfg: elis_config, n_seqs: int, max_seqlen: int) -> int:
+    return lib().elis_pool_head_workspace_bytes(ctypes.byref(cfg), n_seqs, max_seqlen)
+
+
+def elis_pool_head(w: elis_weights, hidden: int, cu_seqlens: int, n_seqs: int, total_tokens: int, max_seqlen: int,
+                   out_pred: int, workspace: int, ws_bytes: int, stream: int | None) -> int:
+    return lib().elis_pool_head(ctypes.byref(w) if w is not None else None, hidden, cu_seqlens, n_seqs,
+                                total_tokens, max_seqlen, out_pred, workspace, ws_bytes, stream)
 
 
 def _tab(t):

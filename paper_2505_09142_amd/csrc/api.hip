@@ -153,6 +153,49 @@ PredictLayout predict_layout(const elis_config& c, int T, int n, int max_seqlen)
     return p;
 }
 
+int check_head(const elis_weights* w) {
+    if (!w) return ELIS_EINVAL;
+    int r = check_config(&w->cfg);
+    if (r != ELIS_OK) return r;
+    if (!w->head_w2 || !w->head_b2) return ELIS_EINVAL;
+    if (w->cfg.head_layers >= 2 && (!w->head_w1 || !w->head_b1)) return ELIS_EINVAL;
+    if (w->cfg.head_layers > 2) {
+        if (!w->head_mid_w || !w->head_mid_b) return ELIS_EINVAL;
+        for (int l = 0; l < w->cfg.head_layers - 2; ++l)
+            if (!w->head_mid_w[l] || !w->head_mid_b[l]) return ELIS_EINVAL;
+    }
+    return ELIS_OK;
+}
+
+// Workspace of elis_pool_head: status word, sequence table, pooling and head scratch.
+struct PoolHeadLayout {
+    size_t status, start, len, tile_off, pool_partial, pool_z, head_hid, total;
+    int nchunk;
+};
+
+PoolHeadLayout pool_head_layout(const elis_config& c, int n, int max_seqlen) {
+    PoolHeadLayout p{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += align_up(bytes);
+        return at;
+    };
+    p.status = take(sizeof(uint32_t));
+    p.start = take(sizeof(int32_t) * n);
+    p.len = take(sizeof(int32_t) * n);
+    p.tile_off = take(sizeof(int32_t) * (n + 1));
+    p.nchunk = (max_seqlen + kPoolChunk - 1) / kPoolChunk;
+    if (c.pooling == ELIS_POOL_MEAN) {
+        p.pool_partial = take(sizeof(float) * static_cast<size_t>(n) * p.nchunk * c.d_model);
+        p.pool_z = take(sizeof(float) * static_cast<size_t>(n) * c.d_model);
+    }
+    if (c.head_layers >= 2)
+        p.head_hid = take(sizeof(float) * static_cast<size_t>(n) * c.head_hidden * (c.head_layers > 2 ? 2 : 1));
+    p.total = o;
+    return p;
+}
+
 size_t attention_ws(int n) {
     return align_up(sizeof(uint32_t)) + 2 * align_up(sizeof(int32_t) * n) + align_up(sizeof(int32_t) * (n + 1));
 }
@@ -357,6 +400,44 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
                             w->head_b2, w->head_mid_w, w->head_mid_b};
         const SeqTable rows{cls_tail ? nullptr : tab.start, tab.len, tab.tile_off};
         return launch_pool_head(head_in, rows, n, d, c.pooling, head, c.out_scale, c.out_shift, out_pred, scr, st);
+    });
+    return status_of(e);
+}
+
+size_t elis_pool_head_workspace_bytes(const elis_config* cfg, int32_t n_seqs, int32_t max_seqlen) {
+    if (check_config(cfg) != ELIS_OK || n_seqs <= 0 || max_seqlen < 1 || max_seqlen > cfg->max_pos) return 0;
+    return pool_head_layout(*cfg, n_seqs, max_seqlen).total;
+}
+
+int elis_pool_head(const elis_weights* w, const float* hidden, const int32_t* cu_seqlens, int32_t n_seqs,
+                   int32_t total_tokens, int32_t max_seqlen, float* out_pred, void* workspace, size_t ws_bytes,
+                   void* stream) {
+    int r = check_head(w);
+    if (r != ELIS_OK) return r;
+    if (!hidden || !cu_seqlens || !out_pred || !workspace) return ELIS_EINVAL;
+    if (n_seqs <= 0 || total_tokens <= 0) return ELIS_EINVAL;
+    if (!aligned(workspace)) return ELIS_EINVAL;
+    const elis_config& c = w->cfg;
+    if (max_seqlen < 1 || max_seqlen > c.max_pos || total_tokens < n_seqs) return ELIS_ESHAPE;
+    const PoolHeadLayout p = pool_head_layout(c, n_seqs, max_seqlen);
+    if (ws_bytes < p.total) return ELIS_EWORKSPACE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int n = n_seqs;
+    const SeqTable tab{at<int32_t>(workspace, p.start), at<int32_t>(workspace, p.len),
+                       at<int32_t>(workspace, p.tile_off)};
+    hipError_t e = timed(ELIS_K_SEQMAP, [&] {
+        return launch_seqmap(cu_seqlens, n, total_tokens, max_seqlen, tab, at<uint32_t>(workspace, p.status), st);
+    });
+    if (e != hipSuccess) return status_of(e);
+    e = timed(ELIS_K_POOL_HEAD, [&] {
+        float* hid = c.head_layers >= 2 ? at<float>(workspace, p.head_hid) : nullptr;
+        const PoolScratch scr{c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_partial) : nullptr,
+                              c.pooling == ELIS_POOL_MEAN ? at<float>(workspace, p.pool_z) : nullptr, hid,
+                              c.head_layers > 2 ? hid + static_cast<size_t>(n) * c.head_hidden : nullptr, p.nchunk};
+        const HeadSpec head{c.head_layers, c.head_hidden, c.head_act, w->head_w1, w->head_b1, w->head_w2,
+                            w->head_b2, w->head_mid_w, w->head_mid_b};
+        return launch_pool_head(hidden, tab, n, c.d_model, c.pooling, head, c.out_scale, c.out_shift, out_pred, scr,
+                                st);
     });
     return status_of(e);
 }

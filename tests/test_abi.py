@@ -285,3 +285,36 @@ def test_job_table_rejects_invalid_arguments(lib):
     assert E.elis_jobs_select_aged(good, FAKE, FAKE, 1.0, 0, 4, FAKE, FAKE, FAKE_WS, ws, None) == E.ELIS_EINVAL
     assert E.elis_jobs_select_aged(good, FAKE, FAKE, 1.0, 10000, 9000, FAKE, FAKE, FAKE_WS, big, None) == \
         E.ELIS_EUNSUPPORTED
+
+
+def test_pool_head_rejects_invalid_arguments(lib):
+    def call(w, hid=FAKE, cu=FAKE, n=4, T=100, msl=64, pred=FAKE, ws=FAKE_WS, wsb=1 << 30):
+        return E.elis_pool_head(w, hid, cu, n, T, msl, pred, ws, wsb, None)
+
+    w = _weights(TINY_HEAD8)
+    cfg = config_of(TINY_HEAD8)
+    need = E.elis_pool_head_workspace_bytes(cfg, 4, 64)
+    assert need > 0 and need % 256 == 0
+    # mean pooling: a partial sum per 64-row chunk of every sequence (one chunk at 64 tokens), the
+    # pooled rows and two hidden buffers
+    d, hh = TINY_HEAD8.d_model, TINY_HEAD8.head_hidden
+    assert need >= 4 * 1 * d * 4 + 4 * d * 4 + 2 * 4 * hh * 4
+    assert E.elis_pool_head_workspace_bytes(cfg, 4, 128) >= need + 4 * d * 4
+    assert E.elis_pool_head_workspace_bytes(cfg, 0, 64) == 0
+    assert E.elis_pool_head_workspace_bytes(cfg, 4, TINY_HEAD8.max_pos + 1) == 0
+    assert call(None) == E.ELIS_EINVAL
+    assert call(w, hid=None) == E.ELIS_EINVAL
+    assert call(w, cu=None) == E.ELIS_EINVAL
+    assert call(w, pred=None) == E.ELIS_EINVAL
+    assert call(w, ws=FAKE_WS + 16) == E.ELIS_EINVAL
+    assert call(w, n=0) == E.ELIS_EINVAL
+    assert call(w, n=8, T=5) == E.ELIS_ESHAPE
+    assert call(w, msl=TINY_HEAD8.max_pos + 1) == E.ELIS_ESHAPE
+    assert call(w, wsb=need - 1) == E.ELIS_EWORKSPACE
+    w.head_mid_b = None
+    assert call(w) == E.ELIS_EINVAL
+    # only the head's pointers are read: encoder pointers may be missing
+    w = _weights(TINY_HEAD8)
+    w.word = None
+    w.layers = None
+    assert call(w, wsb=need - 1) == E.ELIS_EWORKSPACE

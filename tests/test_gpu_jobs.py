@@ -182,3 +182,52 @@ def test_device_scheduler_matches_oracle_trajectory():
          f"(host packing {1e3 * np.median([r.latency_s for r in host.rounds]):.2f} ms)")
     st, bits = dev.drv.table.status()
     assert st == E.ELIS_OK and bits == 0
+
+
+@pytest.mark.parametrize("rescore,end_rule", [("all", "all"), ("pool", "first"), ("all", "first")])
+def test_device_scheduler_rescore_and_window_rules(rescore, end_rule):
+    """The other readings of Alg. 1's loop on the device table: re-scoring every in-flight job each
+    round (rescore "all") and ending a window at the first finish (end_rule "first"). The loop
+    must reproduce the oracle simulator's trajectory under the same rule (packed inputs equal the
+    oracle's inputs, predictions replayed); with "all", every re-scored job whose input did not
+    change gets back its cached prediction bit for bit, so the trajectory equals the Job-Pool one."""
+    s = S_ISRTF
+    W, pr = predictor(s.shape, s.weight_seed)
+    req = make_requests(s)
+    rounds = 60
+    note(f"device loop rescore={rescore} end_rule={end_rule}: {rounds} rounds")
+    dev = _Recorder(DeviceRoundDriver(pr, 1024, s.shape.max_pos))
+    kw = dict(window=s.window, step_cost=s.step_cost_s, batch_cap=s.batch_cap, max_rounds=rounds)
+    got = run_isrtf(req.arrival_t, req.prompt, req.response, dev, rescore=rescore, end_rule=end_rule, **kw)
+    replay = iter([r.pred for r in got.rounds if len(r.rescored)])
+    packed = iter(dev.packed)
+
+    def predict_fn(todo, inputs, g):
+        ids, cu = next(packed)
+        assert np.array_equal(cu, np.concatenate([[0], np.cumsum([len(x) for x in inputs])]))
+        assert np.array_equal(ids, np.concatenate(inputs))
+        return next(replay)
+
+    ref = oracle.simulate(req.arrival_t, req.prompt, req.response, max_pos=s.shape.max_pos, predict_fn=predict_fn,
+                          rescore=rescore, end_rule=end_rule, **kw)
+    assert len(got.rounds) == len(ref.rounds) == rounds
+    for i, (a, b) in enumerate(zip(got.rounds, ref.rounds)):
+        assert a.t == b.t and list(a.rescored) == list(b.rescored), i
+        assert list(a.candidates) == list(b.candidates) and list(a.chosen) == list(b.selected), i
+        assert a.steps == b.window_steps, i
+    assert np.array_equal(got.generated, ref.generated)
+    if rescore == "all":
+        base = run_isrtf(req.arrival_t, req.prompt, req.response, DeviceRoundDriver(pr, 1024, s.shape.max_pos),
+                         rescore="pool", end_rule=end_rule, **kw)
+        cache = {}
+        rekeyed = 0
+        for i, (a, p) in enumerate(zip(got.rounds, base.rounds)):
+            for j, v in zip(p.rescored, p.pred.view(np.uint32)):
+                cache[j] = v
+            assert list(a.chosen) == list(p.chosen) and a.steps == p.steps, i
+            for j, v in zip(a.rescored, a.pred.view(np.uint32)):
+                assert cache[j] == v, (i, j)
+            rekeyed += len(a.rescored) - len(p.rescored)
+        note(f"rescore all: {rekeyed} re-scorings of unchanged jobs, every one bit-identical to the cached key")
+    st, bits = dev.drv.table.status()
+    assert st == E.ELIS_OK and bits == 0
