@@ -67,10 +67,14 @@ def y_rel(p, ref, shape):
 
 def e2e_selection(pred_gpu, pred_ref, arr, k):
     """End-to-end selection check: the GPU's chosen set (GPU select on GPU predictions, equal bit for
-    bit to the oracle select on them) against the oracle select on the oracle's predictions. The
-    two can differ only at a near-tie at the cut, so equality is asserted when the oracle's gap
-    between the k-th and (k+1)-th key exceeds twice the largest prediction error; returns the
-    margin figures either way."""
+    bit to the oracle select on them) against the oracle select on the oracle's predictions.
+
+    With e the largest |p_gpu - p_oracle| and t_k <= t_k+1 the oracle's k-th and (k+1)-th smallest
+    keys, every job with oracle key below t_k - 2e must be chosen by the GPU and every job above
+    t_k+1 + 2e must not be (a job that far from the cut cannot change sides by errors of at most e);
+    this is asserted on every batch. When the gap t_k+1 - t_k exceeds 2e no job is in between, so
+    the two sets must be equal. Returns the margin figures (the jobs inside the band are near-ties
+    whose side the arithmetic does not fix)."""
     pred_gpu = np.asarray(pred_gpu, np.float32)
     pred_ref = np.asarray(pred_ref, np.float64)
     n = len(pred_ref)
@@ -79,13 +83,18 @@ def e2e_selection(pred_gpu, pred_ref, arr, k):
     exp = set(oracle.oracle_select(pred_ref, arr, k).tolist())
     if k >= n or k == 0:
         assert got == exp
-        return dict(gap=float("inf"), max_err=err, margin_ok=True, sets_equal=True)
+        return dict(gap=float("inf"), max_err=err, margin_ok=True, sets_equal=True, near_ties=0)
     srt = np.sort(pred_ref)
+    lo, hi = srt[k - 1] - 2 * err, srt[k] + 2 * err
+    must = set(np.nonzero(pred_ref < lo)[0].tolist())
+    never = set(np.nonzero(pred_ref > hi)[0].tolist())
+    assert must <= got, sorted(must - got)
+    assert not (never & got), sorted(never & got)
     gap = float(srt[k] - srt[k - 1])
     ok = gap > 2 * err
     if ok:
         assert got == exp, (gap, err)
-    return dict(gap=gap, max_err=err, margin_ok=ok, sets_equal=got == exp)
+    return dict(gap=gap, max_err=err, margin_ok=ok, sets_equal=got == exp, near_ties=n - len(must) - len(never))
 
 
 def check_selection(pr, pred_gpu, d_arr, arr, k):
