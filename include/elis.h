@@ -15,7 +15,8 @@
  *  - All data pointers are DEVICE pointers owned by the caller, unless a
  *    comment says "host". The library allocates no device memory, never frees
  *    caller memory and keeps no state between calls (except the opt-in
- *    timing facility at the end of this file).
+ *    timing facility at the end of this file, and the fixed per-device
+ *    scratch of elis_isrtf_select_noalloc).
  *  - Every call validates its scalar arguments on the host, then only
  *    enqueues kernels on `stream` (a hipStream_t; NULL = the default stream)
  *    and returns. Nothing synchronises except elis_read_status and
@@ -177,6 +178,25 @@ size_t elis_select_workspace_bytes(int32_t n);
 int elis_isrtf_select(const float *pred, const int64_t *arrival_seq, int32_t n,
                       int32_t batch_cap, int32_t *out_idx, int32_t *out_count,
                       void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): elis_isrtf_select
+ * without a workspace argument, the same selection bit for bit. Its scratch is
+ * a fixed device array of ELIS_SELECT_NOALLOC_SCRATCH_BYTES inside the library,
+ * one per GPU the library runs on, held until the process ends; its device
+ * address is looked up on the first call on each device. Nothing is allocated
+ * by this call. n <= ELIS_SELECT_NOALLOC_MAX_N (else ELIS_ESHAPE, nothing
+ * enqueued); other arguments, limits and errors as elis_isrtf_select. Every
+ * call on one GPU shares that GPU's scratch, which keeps what the last call
+ * left in it (each call initialises what it reads): calls that can overlap on
+ * one GPU (other streams, other host threads) race, and the caller must order
+ * them.
+ */
+#define ELIS_SELECT_NOALLOC_MAX_N (1 << 18)
+#define ELIS_SELECT_NOALLOC_SCRATCH_BYTES (3u << 20) /* >= elis_select_workspace_bytes(ELIS_SELECT_NOALLOC_MAX_N) */
+int elis_isrtf_select_noalloc(const float *pred, const int64_t *arrival_seq, int32_t n, int32_t batch_cap,
+                              int32_t *out_idx, int32_t *out_count, void *stream);
 
 /*
  * Synchronises `stream`, then reads the device error word that the last call

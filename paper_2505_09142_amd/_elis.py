@@ -87,6 +87,7 @@ SIGNATURES = {
     "elis_select_workspace_bytes": (c_size_t, [c_int32]),
     "elis_isrtf_select": (c_int, [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_void_p, c_size_t,
                                   c_void_p]),
+    "elis_isrtf_select_noalloc": (c_int, [c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p, c_void_p]),
     "elis_read_status": (c_int, [c_void_p, c_void_p, POINTER(c_uint32)]),
     "elis_linear": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p,
                             c_void_p]),
@@ -172,6 +173,15 @@ def elis_select_workspace_bytes(n: int) -> int:
 def elis_isrtf_select(pred: int, arrival_seq: int, n: int, batch_cap: int, out_idx: int, out_count: int,
                       workspace: int, ws_bytes: int, stream: int | None) -> int:
     return lib().elis_isrtf_select(pred, arrival_seq, n, batch_cap, out_idx, out_count, workspace, ws_bytes, stream)
+
+
+ELIS_SELECT_NOALLOC_MAX_N = 1 << 18
+ELIS_SELECT_NOALLOC_SCRATCH_BYTES = 3 << 20
+
+
+def elis_isrtf_select_noalloc(pred: int, arrival_seq: int, n: int, batch_cap: int, out_idx: int, out_count: int,
+                              stream: int | None) -> int:
+    return lib().elis_isrtf_select_noalloc(pred, arrival_seq, n, batch_cap, out_idx, out_count, stream)
 
 
 def elis_read_status(workspace: int, stream: int | None):

@@ -466,6 +466,19 @@ int elis_isrtf_select(const float* pred, const int64_t* arrival_seq, int32_t n, 
     return status_of(e);
 }
 
+int elis_isrtf_select_noalloc(const float* pred, const int64_t* arrival_seq, int32_t n, int32_t batch_cap,
+                              int32_t* out_idx, int32_t* out_count, void* stream) {
+    if (!pred || !arrival_seq || !out_count || (batch_cap > 0 && !out_idx)) return ELIS_EINVAL;
+    if (n <= 0 || batch_cap < 0) return ELIS_EINVAL;
+    if (n > select_noalloc_max_n()) return ELIS_ESHAPE;
+    if ((batch_cap < n ? batch_cap : n) > select_max_k(n)) return ELIS_EUNSUPPORTED;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = timed(ELIS_K_SELECT, [&] {
+        return launch_select_noalloc(pred, arrival_seq, n, batch_cap, out_idx, out_count, st);
+    });
+    return status_of(e);
+}
+
 namespace {
 
 int check_table(const elis_job_table* t) {

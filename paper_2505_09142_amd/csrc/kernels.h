@@ -99,6 +99,13 @@ size_t select_workspace_bytes(int n);
 // workspace: select_workspace_bytes(n) bytes, 256-byte aligned; its first word is the status.
 hipError_t launch_select(const float* pred, const int64_t* arrival, int n, int k, int32_t* out_idx,
                          int32_t* out_count, void* workspace, hipStream_t st);
+// The same selection on the library's fixed per-device scratch (no workspace, no allocation):
+// n <= kNoAllocMaxN jobs; the scratch holds select_workspace_bytes(kNoAllocMaxN).
+constexpr int kNoAllocMaxN = ELIS_SELECT_NOALLOC_MAX_N;
+constexpr size_t kNoAllocScratchBytes = ELIS_SELECT_NOALLOC_SCRATCH_BYTES;
+int select_noalloc_max_n();
+hipError_t launch_select_noalloc(const float* pred, const int64_t* arrival, int n, int k, int32_t* out_idx,
+                                 int32_t* out_count, hipStream_t st);
 
 // jobs.hip: device-resident job table (first token, ring of the last max_pos - 1 tokens,
 // length, cached prediction, arrival) for incremental packing across rounds.

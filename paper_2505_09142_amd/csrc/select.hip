@@ -28,6 +28,8 @@
 //     for ties only.
 #include <limits.h>
 
+#include <mutex>
+
 #include "kernels.h"
 
 namespace elis {
@@ -674,6 +676,53 @@ hipError_t launch_select(const float* pred, const int64_t* arrival, int n, int k
     ELIS_TRY(launch_kernel(select_scatter_kernel, grid, dim3(kBlock), 0, st, pred, n, ws));
     ELIS_TRY(launch_kernel(select_final_kernel, dim3(1), dim3(kThreads), 0, st, pred, arrival, kk, ws, out_idx));
     return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Allocation-free select: the same launches as launch_select on a fixed per-device scratch array
+// instead of a caller workspace. `scratch` below is a device variable: in host code its name is
+// only a stand-in, so the host takes the array's device address once per device with
+// hipGetSymbolAddress and passes that address to the kernels. Each launch sequence initialises
+// what it reads (select_init_kernel writes the selection state and status; every count, list and
+// histogram is stored before it is read), so nothing needs clearing between calls.
+
+namespace {
+
+static_assert(kNoAllocScratchBytes % kAlign == 0, "scratch size");
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each device, once taken
+
+hipError_t scratch_address(void** out) {
+    int dev = 0;
+    ELIS_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        ELIS_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+int select_noalloc_max_n() {
+    static_assert(kNoAllocMaxN <= kLargeMaxN, "limit");
+    return kNoAllocMaxN;
+}
+
+hipError_t launch_select_noalloc(const float* pred, const int64_t* arrival, int n, int k, int32_t* out_idx,
+                                 int32_t* out_count, hipStream_t st) {
+    if (n < 1 || n > kNoAllocMaxN || select_workspace_bytes(n) > kNoAllocScratchBytes) return hipErrorInvalidValue;
+    void* ws = nullptr;
+    ELIS_TRY(scratch_address(&ws));
+    return launch_select(pred, arrival, n, k, out_idx, out_count, ws, st);
 }
 
 }  // namespace elis

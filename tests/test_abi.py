@@ -318,3 +318,25 @@ def test_pool_head_rejects_invalid_arguments(lib):
     w.word = None
     w.layers = None
     assert call(w, wsb=need - 1) == E.ELIS_EWORKSPACE
+
+
+def test_select_noalloc_limits_and_rejections(lib):
+    """The allocation-free select's fixed scratch holds the workspace of its largest n; every
+    invalid call is refused on the host (no device work)."""
+    nmax = E.ELIS_SELECT_NOALLOC_MAX_N
+    assert E.elis_select_workspace_bytes(nmax) <= E.ELIS_SELECT_NOALLOC_SCRATCH_BYTES
+    hdr = open(HEADER).read()
+    assert f"#define ELIS_SELECT_NOALLOC_MAX_N (1 << {nmax.bit_length() - 1})" in hdr
+    assert "#define ELIS_SELECT_NOALLOC_SCRATCH_BYTES (3u << 20)" in hdr
+
+    def call(pred=FAKE, arr=FAKE, n=8, k=4, idx=FAKE, cnt=FAKE):
+        return E.elis_isrtf_select_noalloc(pred, arr, n, k, idx, cnt, None)
+
+    assert call(pred=None) == E.ELIS_EINVAL
+    assert call(arr=None) == E.ELIS_EINVAL
+    assert call(cnt=None) == E.ELIS_EINVAL
+    assert call(idx=None) == E.ELIS_EINVAL
+    assert call(n=0) == E.ELIS_EINVAL
+    assert call(k=-1) == E.ELIS_EINVAL
+    assert call(n=nmax + 1) == E.ELIS_ESHAPE
+    assert call(n=nmax, k=8193) == E.ELIS_EUNSUPPORTED
