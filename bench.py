@@ -104,15 +104,13 @@ _GEMM_EPI = {"gemm_qkv": (0, 0), "gemm_o": (2, 4), "gemm_ffn1": (1, 1), "gemm_ff
 
 def _gemm_kernel(bm, bn, wgs, epi, n, f32):
     if (bm, bn) == (256, 256):
-        return f"gemm_sched_kernel<256, 256, 2, 4, 32, {epi}, 64, 1, 2>"
+        return f"gemm_sched_kernel<256, 256, 2, 4, 32, {epi}, 1, 2>"
     if (bm, bn) == (128, 128):
-        if not f32 and n % 256:
-            return f"gemm_dlds_kernel<128, 128, 2, 2, 32, 2, {epi}, 64>"
-        return f"gemm_sched_kernel<128, 128, 2, 2, 32, {epi}, 64, 2, 2>"
+        return f"gemm_sched_kernel<128, 128, 2, 2, 32, {epi}, 2, 2>"
     if (bm, bn) == (64, 128):
-        return f"gemm_sched_kernel<64, 128, 2, 2, 32, {epi}, 64, {wgs}, {2 if wgs == 2 else 4}>"
+        return f"gemm_sched_kernel<64, 128, 2, 2, 32, {epi}, {wgs}, {2 if wgs == 2 else 4}>"
     if (bm, bn) == (64, 64):
-        return f"gemm_sched_kernel<64, 64, 2, 2, 32, {epi}, 64, {wgs}, {2 if wgs == 4 else 4}>"
+        return f"gemm_sched_kernel<64, 64, 2, 2, 32, {epi}, {wgs}, {2 if wgs == 4 else 4}>"
     return f"gemm_kernel<128, 64, 2, 2, 16, {epi}>"
 
 

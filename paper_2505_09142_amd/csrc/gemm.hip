@@ -33,11 +33,14 @@
 // XCD runs together share activation rows and weight columns in its L2.
 #include <type_traits>
 
+#include "gemm_common.h"
 #include "kernels.h"
 
 namespace elis {
 
 namespace {
+
+using namespace gemm;
 
 constexpr int kBK = 64;
 
@@ -60,12 +63,6 @@ __device__ __forceinline__ f32x4 residual4(const Residual& res, f32x4 h, int m, 
     return h;
 }
 
-__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
-    constexpr int kXcd = 8;
-    const int per = nblk / kXcd, rem = nblk % kXcd;
-    const int xcd = bid % kXcd, local = bid / kXcd;
-    return xcd * per + (xcd < rem ? xcd : rem) + local;
-}
 
 // LDS chunk swizzle of the direct-to-LDS kernels: physical 16-byte chunk = logical chunk ^ swz(row).
 // Measured free of bank conflicts on gfx950 for both 16-row and 32-row fragment reads (the
@@ -88,29 +85,6 @@ __device__ __forceinline__ float gelu_erf(float x) {
     return fmaf(-a, __builtin_amdgcn_exp2f(q), fmaxf(x, 0.f));
 }
 
-// One MFMA block of the wave tile: MI x MI outputs (MI = 16: 16x16x32, MI = 32: 32x32x16).
-template <int MI>
-struct Mfma;
-
-template <>
-struct Mfma<16> {
-    typedef f32x4 acc_t;
-    static constexpr int kRegs = 4;
-    static constexpr int kDepth = 32;  // k per instruction
-    __device__ static __forceinline__ acc_t run(bf16x8 a, bf16x8 b, acc_t c) {
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-    }
-};
-
-template <>
-struct Mfma<32> {
-    typedef f32x16 acc_t;
-    static constexpr int kRegs = 16;
-    static constexpr int kDepth = 16;
-    __device__ static __forceinline__ acc_t run(bf16x8 a, bf16x8 b, acc_t c) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-    }
-};
 
 template <int BM, int BN, int WM, int WN, int MI, int EPI>
 __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __restrict__ A,
@@ -253,26 +227,6 @@ __global__ __launch_bounds__(WM* WN* kWave) void gemm_kernel(const uint16_t* __r
 // barrier that follows makes every thread's part of that slab visible and also guarantees
 // that every wave has finished reading the stage the next loads will overwrite.
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    // gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits 15:14; expcnt/lgkmcnt left at max.
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// One wave-wide 16-byte-per-lane load from global memory straight into LDS: lane i's 16 bytes
-// land at lds + 16 * i.
-__device__ __forceinline__ void load_lds_16(const void* src, void* lds) {
-    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)lds, 16, 0, 0);
-}
-
-__device__ __forceinline__ void block_sync_lds() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-}
 
 // Tile index -> (tile row, tile col), grouping GM tile rows so that the tiles running
 // together on one XCD share a small set of A rows and B columns (L2 reuse).
@@ -298,23 +252,6 @@ __device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, in
 // conflicts on gfx950 for both the 16-row (16x16x32) and 32-row (32x32x16) fragment reads;
 // the plain (row & 7) form conflicts 4-way on the 32-row reads.
 
-template <int N>
-__device__ __forceinline__ void wait_lgkm() {
-    __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (N << 8) | (3 << 14));
-}
-
-// NM MFMA groups, with NV direct loads and ND LDS reads spread evenly in front of them.
-template <int G, int NM, int NV, int ND, int SYNC>
-__device__ __forceinline__ void interleave_step() {
-    if constexpr (G < NM) {
-        constexpr int v = (G + 1) * NV / NM - G * NV / NM;
-        constexpr int d = (G + 1) * ND / NM - G * ND / NM;
-        if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, SYNC);
-        if constexpr (d > 0) __builtin_amdgcn_sched_group_barrier(0x100, d, SYNC);
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, SYNC);
-        interleave_step<G + 1, NM, NV, ND, SYNC>();
-    }
-}
 
 template <int BM, int BN, int WM, int WN, int MI, int EPI, int OCC = 1, int S = 2>
 __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void gemm_sched_kernel(
