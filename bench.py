@@ -53,34 +53,46 @@ def _describe(w):
 
 
 def _algorithmic(w, b):
-    """Algorithmic FLOPs (contractions) or bytes (row kernels) by kernel class: (kind, average per
-    launch, launches per step). With CLS pooling the last layer needs, after its QKV product, only
-    the CLS rows (one attention query and one row of every later product per sequence); that is
-    all the library computes there, and all that is counted."""
+    """Algorithmic FLOPs (contractions) or bytes (row kernels) by kernel class: (kind, the work of
+    each launch of one step in launch order, launches per step). With CLS pooling the last layer
+    needs, after its QKV product, only the CLS rows (one attention query and one row of every later
+    product per sequence); that is all the library computes there, and all that is counted."""
     s = w.shape
     T, n, d, F, L = b.total, b.n, s.d_model, s.d_ff, s.n_layers
     lens = b.lengths.astype(float)
     sumsq = float((lens ** 2).sum())
     cls_tail = s.pooling == 0 and L > 0
-    rows = (L - 1) * T + n if cls_tail else L * T          # rows through the post-attention layers
-    att = 4.0 * d * ((L - 1) * sumsq + float(lens.sum())) if cls_tail else 4.0 * d * L * sumsq
+    rows = [T] * L
+    att = [4.0 * d * sumsq] * L
+    if cls_tail:
+        rows[-1] = n
+        att[-1] = 4.0 * d * float(lens.sum())
     # fp32 row in; bf16 row + (mean, rstd) out (the last LayerNorm writes an fp32 row instead:
     # counted as the common case)
     ln_row = d * (4.0 + 2.0) + 8.0
-    return {
-        "gemm_qkv": ("flop", 2.0 * T * d * 3 * d, L),
-        "attention": ("flop", att / L, L),
-        "gemm_o": ("flop", 2.0 * rows * d * d / L, L),
-        "gemm_ffn1": ("flop", 2.0 * rows * d * F / L, L),
-        "gemm_ffn2": ("flop", 2.0 * rows * F * d / L, L),
-        "layernorm": ("byte", 2 * rows * ln_row / (2 * L), 2 * L),
+    ln = [r * ln_row for r in rows for _ in (0, 1)]  # after the out-projection and after FFN2
+    alg = {
+        "gemm_qkv": ("flop", [2.0 * T * d * 3 * d] * L),
+        "attention": ("flop", att),
+        "gemm_o": ("flop", [2.0 * r * d * d for r in rows]),
+        "gemm_ffn1": ("flop", [2.0 * r * d * F for r in rows]),
+        "gemm_ffn2": ("flop", [2.0 * r * F * d for r in rows]),
+        "layernorm": ("byte", ln),
         # ids + gathered bf16 word and position rows in; fp32 pre-norm + bf16 rows + stats out
-        "embed_ln": ("byte", T * (4.0 + d * (2.0 + 2.0 + 4.0 + 2.0) + 8.0), 1),
+        "embed_ln": ("byte", [T * (4.0 + d * (2.0 + 2.0 + 4.0 + 2.0) + 8.0)]),
         # the hidden rows pooling reads (CLS: one per sequence; mean: every token) + every head weight once
-        "pool_head": ("byte", (n if s.pooling == 0 else T) * d * 4.0 + 4.0 * _head_params(s), 1),
-        "seqmap": ("byte", (n + 1) * 4.0 * 4, 1),
-        "select": ("byte", n * 12.0 + w.batch_cap * 4.0, 1),
+        "pool_head": ("byte", [(n if s.pooling == 0 else T) * d * 4.0 + 4.0 * _head_params(s)]),
+        "seqmap": ("byte", [(n + 1) * 4.0 * 4]),
+        "select": ("byte", [n * 12.0 + w.batch_cap * 4.0]),
     }
+    return {k: (kind, per, len(per)) for k, (kind, per) in alg.items() if per}
+
+
+def sampled_work(per_launch, stride, launches):
+    """Average work of the launches a stride-`stride` sample timed: launch j = stride * i of the
+    class since the reset, i < launches, is launch j mod (launches per step) of its step."""
+    m = len(per_launch)
+    return sum(per_launch[(stride * i) % m] for i in range(launches)) / launches
 
 
 def _source_sha(paths):
@@ -97,8 +109,8 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "bert_base_b64_hbm_traffic.md")
 # is reported only while those sources are unchanged. A GEMM class is one launch or two (the
 # library's launch plan may split the rows between a large-tile and a small-tile launch); the
 # plan comes from elis_linear_plan at the workload's token count.
-_GEMM_SRC = ["paper_2505_09142_amd/csrc/gemm.hip", "paper_2505_09142_amd/csrc/common.h",
-             "paper_2505_09142_amd/csrc/kernels.h"]
+_GEMM_SRC = ["paper_2505_09142_amd/csrc/gemm.hip", "paper_2505_09142_amd/csrc/gemm_common.h",
+             "paper_2505_09142_amd/csrc/common.h", "paper_2505_09142_amd/csrc/kernels.h"]
 _GEMM_EPI = {"gemm_qkv": (0, 0), "gemm_o": (2, 4), "gemm_ffn1": (1, 1), "gemm_ffn2": (2, 5)}  # public, internal
 
 
@@ -1212,7 +1224,10 @@ def main():
         s_, nl, ms = E.elis_timing_read(E.K[name])
         if nl == 0:
             continue
-        kind, per_launch, _ = alg[name]
+        kind, per, count = alg[name]
+        if nl != count * args.steps:
+            raise SystemExit(f"{name}: {nl} launches in {args.steps} steps, the work model expects {count} per step")
+        per_launch = sum(per) / count
         avg_s = ms / nl * 1e-3
         rate = per_launch / avg_s / (1e12 if kind == "flop" else 1e9)
         kernels[name] = {"launches_per_step": nl / args.steps, "avg_us": avg_s * 1e6, "ms_per_step": ms / args.steps,
@@ -1246,16 +1261,17 @@ def main():
     if st != E.ELIS_OK:
         raise SystemExit(f"device status {st} bits {bits}")
 
-    kind, per_launch, _ = alg[dominant]
+    kind, per, _ = alg[dominant]
+    per_launch = sampled_work(per, stride, dl)   # the work of exactly the launches the sample timed
     avg_s = dms / dl * 1e-3
     if kind == "flop":
         achieved, peak, unit, bound = per_launch / avg_s / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s", "mfma"
     else:
         achieved, peak, unit, bound = per_launch / avg_s / 1e9, PEAK_HBM_GBS, "GB/s", "hbm"
-    gemm_flop = sum(alg[k][1] * alg[k][2] for k in ("gemm_qkv", "gemm_o", "gemm_ffn1", "gemm_ffn2"))
+    gemm_flop = sum(sum(alg[k][1]) for k in ("gemm_qkv", "gemm_o", "gemm_ffn1", "gemm_ffn2"))
     gemm_s = sum(kernels[k]["ms_per_step"] for k in ("gemm_qkv", "gemm_o", "gemm_ffn1", "gemm_ffn2")) * 1e-3
     att_s = kernels["attention"]["ms_per_step"] * 1e-3
-    att_flop = alg["attention"][1] * alg["attention"][2]
+    att_flop = sum(alg["attention"][1])
 
     out = {
         "metric": "predicted seqs/sec + tokens/sec per round; MFMA util; p50 predict+select latency",
@@ -1284,9 +1300,49 @@ def main():
                      "avg_launch_us": avg_s * 1e6, "launches": dl, "timing_stride": stride},
         "kernels": kernels,
     }
+    if args.workload == "bert_base_b64":
+        out["b256_round0"] = b256_round0(pr)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, W, b, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def b256_round0(pr, passes=5):
+    """The batch-256 workload's first round (the same BERT-base predictor weights; 256 sequences,
+    ~92K tokens), outside the timed steps: per-class kernel time of a few predictor passes, so the
+    GEMM and attention matrix-core utilisation at that size comes with every bench line."""
+    import torch
+    from paper_2505_09142_amd import _elis as E
+    from paper_2505_09142_amd.device import upload_batch
+    from workloads import W_BERT_B256_ROUNDS
+    from workloads.gen import RoundStream
+    w = W_BERT_B256_ROUNDS
+    b = RoundStream(w).batch(0)
+    ids, cu, arr = upload_batch(b, pr.device)
+    pred = torch.empty(b.n, dtype=torch.float32, device=pr.device)
+    for _ in range(2):
+        pr.predict(ids, cu, b.max_seqlen, out_pred=pred)
+    torch.cuda.synchronize()
+    alg = _algorithmic(w, b)
+    E.elis_timing_reset()
+    E.elis_timing_enable((1 << len(E.KERNEL_CLASSES)) - 1)
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for _ in range(passes):
+        pr.predict(ids, cu, b.max_seqlen, out_pred=pred)
+    a1.record()
+    torch.cuda.synchronize()
+    E.elis_timing_enable(0)
+    cls_ms = {name: E.elis_timing_read(E.K[name])[2] / passes for name in E.KERNEL_CLASSES}
+    E.elis_timing_reset()
+    gemm = ("gemm_qkv", "gemm_o", "gemm_ffn1", "gemm_ffn2")
+    gemm_flop = sum(sum(alg[k][1]) for k in gemm)
+    gemm_ms = sum(cls_ms[k] for k in gemm)
+    return {"workload": f"{w.name} round 0: {b.n} sequences, {b.total} tokens, predict only",
+            "total_tokens": int(b.total), "ms_per_pass_timed_classes": a0.elapsed_time(a1) / passes,
+            "mfma_util_gemm": gemm_flop / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "mfma_util_attention": sum(alg["attention"][1]) / (cls_ms["attention"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "gemm_tflops": {k: sum(alg[k][1]) / (cls_ms[k] * 1e-3) / 1e12 for k in gemm}}
 
 
 if __name__ == "__main__":

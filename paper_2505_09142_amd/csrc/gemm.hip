@@ -31,6 +31,7 @@
 // to the 8 XCDs (each with its own L2). Ids are remapped so every XCD gets one
 // contiguous range of tiles, grouped GROUP_M tile rows at a time: the tiles an
 // XCD runs together share activation rows and weight columns in its L2.
+#include <atomic>
 #include <type_traits>
 
 #include "gemm_common.h"
@@ -577,17 +578,18 @@ int gemm_config_of_tile(int bm, int bn, int wgs_per_cu) {
     return -1;
 }
 
-// Compute units of the current device (cached per device; the launch-time model below needs it).
+// Compute units of the current device (the launch-time model below needs it). A device property,
+// looked up once per device; the cache is safe to read and fill from several host threads.
 int device_cus() {
-    static int cus[64];
+    static std::atomic<int> cus[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cus[dev] == 0) {
-        int v = 0;
+    int v = cus[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-        cus[dev] = v;
+        cus[dev].store(v, std::memory_order_relaxed);
     }
-    return cus[dev];
+    return v;
 }
 
 namespace {

@@ -10,6 +10,11 @@
 // statistics (mean, rstd) instead of an fp32 copy: the fp32-output GEMM that
 // consumes the row as its residual rebuilds y = fmaf((z - mean) * rstd, g, b)
 // from the pre-norm row z, which saves writing and re-reading an fp32 copy.
+// Floating-point contraction is off in the row finish: every product and sum is
+// rounded as written (only the explicit fmaf is fused), so the normalised row it
+// writes is exactly what that rebuild computes from the stored mean and rstd (with
+// contraction the compiler fused the mean into z - mean and the variance into
+// var + eps, and the two sides could differ in the last bit).
 #include "kernels.h"
 
 namespace elis {
@@ -21,6 +26,7 @@ constexpr int kRowsPerBlock = 4;  // 4 waves, one row each
 template <int VPL>
 __device__ __forceinline__ void ln_finish(f32x4 (&v)[VPL], int lane, int d, const float* __restrict__ g,
                                           const float* __restrict__ b, float eps, size_t row, const LnOut& o) {
+#pragma clang fp contract(off)
     float* o32 = o.y32 ? o.y32 + row * d : nullptr;
     uint16_t* o16 = o.y16 ? o.y16 + row * d : nullptr;
     float s = 0.f;
