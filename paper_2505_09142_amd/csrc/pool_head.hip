@@ -12,9 +12,15 @@
 //   pool_partial  mean pooling only: per (sequence, 256-column block, 64-row
 //                 chunk) column sums, fully coalesced row reads;
 //   pool_reduce   mean pooling only: chunk sums in order, divided by the length;
-//   head_fc       every layer of a multi-layer head but the last: one wave per
-//                 (output unit, 8 sequences), lanes across the inputs,
-//                 ping-ponging between two [n, hidden] buffers;
+//   head_tile     every layer of a multi-layer head but the last, when the inputs
+//                 are a multiple of 64 and the outputs of 16 (every configured
+//                 head): one work-group per 16 sequences x 16 output units, its
+//                 4 or 8 waves splitting the inputs, each accumulating its part on
+//                 the fp32 matrix cores (16 x 16 x 4 blocks); the parts are summed
+//                 in a fixed order through LDS. Ping-pongs between two [n, hidden]
+//                 buffers;
+//   head_fc       the same layer for other widths: one wave per (output unit,
+//                 8 sequences), lanes across the inputs;
 //   head_out      one wave per sequence: ReLU(hidden + b1) . w2 + b2 (or z . w
 //                 + b for the linear head), then shift + scale * y.
 // For CLS pooling the head reads the CLS row of the hidden states in place.
@@ -67,8 +73,18 @@ __global__ __launch_bounds__(kCols) void pool_reduce_kernel(const float* __restr
     const int L = len[s];
     const int used = (L + kPoolChunk - 1) / kPoolChunk;
     const float* p = partial + static_cast<size_t>(s) * nchunk * d + c;
+    const int m = used < nchunk ? used : nchunk;
+    // Chunk sums in chunk order; eight loads in flight per pass.
+    constexpr int kU = 8;
     float acc = 0.f;
-    for (int ch = 0; ch < used && ch < nchunk; ++ch) acc += p[static_cast<size_t>(ch) * d];
+    for (int c0 = 0; c0 < m; c0 += kU) {
+        float v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) v[u] = c0 + u < m ? p[static_cast<size_t>(c0 + u) * d] : 0.f;
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            if (c0 + u < m) acc += v[u];
+    }
     z[static_cast<size_t>(s) * d + c] = acc / static_cast<float>(L);
 }
 
@@ -118,6 +134,68 @@ __global__ __launch_bounds__(kWave) void head_fc_kernel(const float* __restrict_
     }
 }
 
+// One fully connected layer, out[s, j] = act(x[s, :] . w[j, :] + b[j]), on the fp32 matrix cores.
+// A work-group owns 16 sequences x 16 output units; its NW waves split the K inputs into
+// contiguous quarters (eighths). Per 16 inputs a lane loads 4 consecutive inputs of its row and
+// of its weight row (16 bytes each) and issues four 16 x 16 x 4 blocks; lane l supplies input
+// k0 + 4 (l / 16) + i of row l % 16 to block i, the same k for both operands, so every block
+// multiplies matching inputs and the 16 inputs are covered once. A wave's 16 x 16 part sits in
+// the accumulator layout (lane l: sequences 4 (l / 16) + {0..3}, unit l % 16); the parts are
+// summed through LDS in wave order, the bias added and the activation applied by wave 0.
+// Every output depends on its own sequence's row only, in a fixed order: results do not depend
+// on how many sequences are batched. grid (N / 16, ceil(n / 16)), NW waves; K % (16 NW) == 0.
+template <int ACT, bool POOLED, int NW>
+__global__ __launch_bounds__(NW* kWave) void head_tile_kernel(const float* __restrict__ in,
+                                                              const float* __restrict__ hidden,
+                                                              const float* __restrict__ z,
+                                                              const int32_t* __restrict__ start, int pooling, int n,
+                                                              int K, int N, const float* __restrict__ w,
+                                                              const float* __restrict__ b, float* __restrict__ out) {
+    __shared__ f32x4 part[NW][kWave];
+    const int o0 = blockIdx.x * 16, s0 = blockIdx.y * 16;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wv = tid / kWave;
+    const int r = lane & 15, kq = lane >> 4;
+    const int s = s0 + r < n ? s0 + r : n - 1;  // rows past the end repeat the last, stored nowhere
+    const float* xr = POOLED ? pooled_row(s, pooling, hidden, z, start, K) : in + static_cast<size_t>(s) * K;
+    const float* wr = w + static_cast<size_t>(o0 + r) * K;
+    // Up to kBatch steps of 16 inputs per pass: all their loads are issued before the first block
+    // (a wave's share of K is short, so the pass is bound by one load latency, not by a chain).
+    constexpr int kBatch = 8;
+    const int kw = K / NW, steps = kw / 16;  // the step count is the same for every lane
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int m0 = 0; m0 < steps; m0 += kBatch) {
+        const int k0 = wv * kw + 16 * m0 + 4 * kq;
+        f32x4 xv[kBatch], wq[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (m0 + u < steps) {
+                xv[u] = *reinterpret_cast<const f32x4*>(xr + k0 + 16 * u);
+                wq[u] = *reinterpret_cast<const f32x4*>(wr + k0 + 16 * u);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (m0 + u < steps) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(xv[u][i], wq[u][i], acc, 0, 0, 0);
+            }
+        }
+    }
+    part[wv][lane] = acc;
+    __syncthreads();
+    if (wv != 0) return;
+    f32x4 t = part[0][lane];
+#pragma unroll
+    for (int q = 1; q < NW; ++q) t += part[q][lane];
+    const int o = o0 + r;
+    const float bo = b[o];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int si = s0 + 4 * kq + i;
+        if (si < n) out[static_cast<size_t>(si) * N + o] = act<ACT>(t[i] + bo);
+    }
+}
+
 // grid (n), one wave per work-group.
 __global__ __launch_bounds__(kWave) void head_out_kernel(const float* __restrict__ hidden,
                                                          const float* __restrict__ z,
@@ -128,8 +206,20 @@ __global__ __launch_bounds__(kWave) void head_out_kernel(const float* __restrict
     const int s = blockIdx.x, lane = threadIdx.x;
     const float* x = hh > 0 ? hid + static_cast<size_t>(s) * hh : pooled_row(s, pooling, hidden, z, start, d);
     const int len = hh > 0 ? hh : d;
+    // Eight strided elements per lane per pass, all loaded before the first product.
+    constexpr int kU = 8;
     float acc = 0.f;
-    for (int c = lane; c < len; c += kWave) acc += x[c] * w2[c];
+    for (int c0 = lane; c0 < len; c0 += kU * kWave) {
+        float xv[kU], wv[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int c = c0 + u * kWave;
+            xv[u] = c < len ? x[c] : 0.f;
+            wv[u] = c < len ? w2[c] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) acc = fmaf(xv[u], wv[u], acc);
+    }
     const float y = wave_sum(acc) + b2[0];
     if (lane == 0) out[s] = shift + scale * y;
 }
@@ -141,8 +231,16 @@ namespace {
 template <int ACT, bool POOLED>
 hipError_t fc(const float* in, const float* hidden, const float* z, const int32_t* start, int pooling, int n, int K,
               int N, const float* w, const float* b, float* out, hipStream_t st) {
-    ELIS_TRY(launch_kernel((head_fc_kernel<ACT, POOLED>), dim3(N, (n + kFcSeq - 1) / kFcSeq), dim3(kWave), 0, st, in,
-                       hidden, z, start, pooling, n, K, N, w, b, out));
+    if (N % 16 == 0 && K % 128 == 0) {
+        ELIS_TRY(launch_kernel((head_tile_kernel<ACT, POOLED, 8>), dim3(N / 16, (n + 15) / 16), dim3(8 * kWave), 0, st,
+                               in, hidden, z, start, pooling, n, K, N, w, b, out));
+    } else if (N % 16 == 0 && K % 64 == 0) {
+        ELIS_TRY(launch_kernel((head_tile_kernel<ACT, POOLED, 4>), dim3(N / 16, (n + 15) / 16), dim3(4 * kWave), 0, st,
+                               in, hidden, z, start, pooling, n, K, N, w, b, out));
+    } else {
+        ELIS_TRY(launch_kernel((head_fc_kernel<ACT, POOLED>), dim3(N, (n + kFcSeq - 1) / kFcSeq), dim3(kWave), 0, st,
+                               in, hidden, z, start, pooling, n, K, N, w, b, out));
+    }
     return hipSuccess;
 }
 
