@@ -490,6 +490,10 @@ HEAD_CASES = [
     (TINY_CLS_LIN8, [4] * 37),
     (BERT_BASE_HEAD8, [1, 64, 65, 129, 512, 300, 17] * 10),
     (dataclasses.replace(BERT_BASE, name="bert_base_mean_linear", pooling=1, head_hidden=0), [1, 64, 65, 511, 7]),
+    # widths off the matrix-core tile: 20 (no layer is a multiple of 16 units: every hidden layer on
+    # the one-wave-per-unit kernel) and 48 (the first layer on the tile, the 48-input middle layers not)
+    (dataclasses.replace(TINY_HEAD8, name="tiny_head8_w20", head_hidden=20), [16, 1, 64, 37, 5]),
+    (dataclasses.replace(TINY_HEAD8, name="tiny_head8_w48", head_hidden=48), [16, 1, 64, 37, 5, 19, 33]),
 ]
 
 
