@@ -23,11 +23,15 @@
 // the output is normalised by exactly the weights it was built from.
 //
 // LDS. K is stored row-major with 16-byte chunks XOR-swizzled by row pairs
-// (the 16 rows one fragment read touches then cover every bank once); V is
-// stored transposed (V^T[d][key], rows padded to 72 keys, keys permuted within each
-// 32-key chunk, see vt_pos) so that a lane's 8 keys for one d are one 16-byte read. Two LDS buffers: the next tile is
-// fetched from HBM into registers while the current one is multiplied, so
-// each tile costs one barrier and its load latency is hidden.
+// (the 16 rows one fragment read touches then cover every bank once). With d_head 64,
+// V is stored row-major too, its 8-byte units XOR-swizzled by row pairs, and the
+// V^T operand is read with ds_read_b64_tr_b16, which transposes 4x4 blocks of bf16
+// across the lanes of a 16-lane group; both tiles go from HBM straight into LDS with
+// no register staging. With d_head 32, V is staged through registers and stored
+// transposed (V^T[d][key], rows padded to 72 keys, keys permuted within each 32-key
+// chunk, see vt_pos) so that a lane's 8 keys for one d are one 16-byte read. Two LDS
+// buffers: the next tile is in flight while the current one is multiplied, so each
+// tile costs one barrier and its load latency is hidden.
 #include <math.h>
 
 #include "kernels.h"
@@ -60,6 +64,16 @@ __device__ __forceinline__ int vt_pos(int k) {
     return (k & ~31) | (((k >> 2) & 3) << 3) | (((k >> 4) & 1) << 2) | (k & 3);
 }
 
+// Row-major V tile (d_head 64, 128-byte rows): physical 8-byte unit = logical unit ^ vswz(row).
+// The transposed reads of one 16-lane group touch rows 4a + {0..3} and four consecutive units,
+// and the rows of a pair share a mask: with the mask moving a whole 4-unit block per row pair,
+// the 32 lanes of two groups cover all 64 banks once.
+__device__ __forceinline__ int vswz_m(int row) { return (row >> 1) & 3; }  // in 4-unit blocks
+__device__ __forceinline__ int vswz(int row) { return vswz_m(row) << 2; }   // in 8-byte units
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __attribute__((address_space(3))) const uint16_t lds_cu16;
+
 // Maximum over the lanes l, l^16, l^32, l^48 (the four lanes that hold one query's scores).
 __device__ __forceinline__ float quad_max(float v) {
     const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -74,12 +88,19 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                                                                   const int32_t* __restrict__ seq_len,
                                                                   const int32_t* __restrict__ tile_off, int n,
                                                                   int H, uint16_t* __restrict__ out,
-                                                                  float scale_log2, int cls_only) {
+                                                                  float scale_log2, int cls_only, int total) {
+// The body is device code only: the host pass has no buffer-resource type, and a kernel whose
+// body it cannot form would lose its host-side launch stub.
+#if defined(__HIP_DEVICE_COMPILE__)
     constexpr int CPR = DH / 8;   // 16-byte chunks per head row
     constexpr int KS = DH / 32;   // MFMA k-steps over d_head
     constexpr int DT = DH / 16;   // 16-wide d blocks of the output
     __shared__ __attribute__((aligned(16))) uint16_t sK[2 * kBKV * DH];
-    __shared__ __attribute__((aligned(16))) uint16_t sVt[2 * DH * kVtStride];
+    // d_head 64: V tiles row-major (8-byte units XOR-swizzled by row pair, see vswz), read back
+    // transposed by ds_read_b64_tr_b16; d_head 32: V^T rows staged through registers (vt_pos).
+    constexpr bool VDIRECT = DH == 64;
+    constexpr int VBUF = VDIRECT ? kBKV * DH : DH * kVtStride;
+    __shared__ __attribute__((aligned(16))) uint16_t sVt[2 * VBUF];
 
     const int tile = blockIdx.x, h = blockIdx.y;
     // cls_only: one work-group per (sequence, head) computing the first 32 queries (wave 0,
@@ -123,22 +144,82 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 #pragma unroll
     for (int e = 0; e < 8; ++e) ones[e] = static_cast<__bf16>(1.0f);
 
-    // Staging of one 64-key tile: K as 16-byte row chunks, V as pairs of rows (2 keys x 8 d).
-    constexpr int KCH = kBKV * CPR;                 // K chunks per tile
+    // Staging of one 64-key tile. K goes from global memory straight into its LDS buffer
+    // (direct-to-LDS loads, no registers): a wave-wide 16-byte load fills 64 / CPR consecutive
+    // K rows, lane i writing the 16 bytes at offset 16 i, so lane i fetches the logical chunk
+    // that the row swizzle places there; wave w fills rows [16 w, 16 w + 16). With d_head 64, V
+    // takes the same route into a row-major tile; with d_head 32 it goes through registers as
+    // pairs of rows (2 keys x 8 d) and is transposed into V^T on the way to LDS.
+    // A tile wholly inside the sequence is addressed through a buffer resource over the packed
+    // qkv rows (per-thread offsets of the first tile's rows plus the tile start as a scalar
+    // offset, no per-tile address arithmetic); the sequence's last tile clamps its rows to the
+    // last token, so no key or value of another sequence is ever read.
     constexpr int VCH = (kBKV / 2) * CPR;           // V units per tile
-    constexpr int KPT = (KCH + kWaves * kWave - 1) / (kWaves * kWave);
     constexpr int VPT = (VCH + kWaves * kWave - 1) / (kWaves * kWave);
-    u32x4 rk[KPT], rv0[VPT], rv1[VPT];
-    auto gload = [&](int kv0) {
+    constexpr int KRL = kWave / CPR;                // K rows per direct load
+    constexpr int KLW = 16 / KRL;                   // direct loads per wave per tile
+    static_assert(KLW * KRL * kWaves == kBKV, "each wave fills 16 K rows");
+    u32x4 rv0[VPT], rv1[VPT];
+    const int wsc = __builtin_amdgcn_readfirstlane(wid);
+    const bool offs32 = static_cast<size_t>(total) * D3 * 2 < (1ull << 31);
+    const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(qkv), 0, offs32 ? total * D3 * 2 : 0, 0x00020000);
+    int krow[KLW], kch[KLW], vch[KLW];
+    uint32_t okb[KLW], ovd[KLW], ovb[VPT];
 #pragma unroll
-        for (int i = 0; i < KPT; ++i) {
-            const int c = tid + i * kWaves * kWave;
-            if (KCH % (kWaves * kWave) == 0 || c < KCH) {
-                const int row = c / CPR, ch = c % CPR;
-                int tok = kv0 + row;
-                tok = tok < L ? tok : L - 1;
-                rk[i] = *reinterpret_cast<const u32x4*>(Kg + static_cast<size_t>(seq0 + tok) * D3 + ch * 8);
+    for (int i = 0; i < KLW; ++i) {
+        krow[i] = wsc * 16 + i * KRL + lane / CPR;
+        kch[i] = (lane % CPR) ^ kswz<DH>(krow[i]);
+        okb[i] = static_cast<uint32_t>(((seq0 + krow[i]) * D3 + D + h * DH + kch[i] * 8) * 2);
+        vch[i] = (lane % CPR) ^ (vswz(krow[i]) >> 1);  // 16-byte chunk: the 8-byte swizzle in pairs
+        ovd[i] = static_cast<uint32_t>(((seq0 + krow[i]) * D3 + 2 * D + h * DH + vch[i] * 8) * 2);
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+        const int u = tid + i * kWaves * kWave;
+        ovb[i] = static_cast<uint32_t>(((seq0 + 2 * (u % (kBKV / 2))) * D3 + 2 * D + h * DH + (u / (kBKV / 2)) * 8) * 2);
+    }
+    typedef __attribute__((address_space(3))) void lds_t;
+    auto gload = [&](int kv0, int b) {
+        uint16_t* k_s = sK + b * (kBKV * DH) + wsc * 16 * DH;
+        if (offs32 && kv0 + kBKV <= L) {
+            const int so = kv0 * D3 * 2;
+#pragma unroll
+            for (int i = 0; i < KLW; ++i)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_t*)(k_s + i * KRL * DH), 16, okb[i], so, 0, 0);
+            if constexpr (VDIRECT) {
+                uint16_t* v_d = sVt + b * VBUF + wsc * 16 * DH;
+#pragma unroll
+                for (int i = 0; i < KLW; ++i)
+                    __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_t*)(v_d + i * KRL * DH), 16, ovd[i], so, 0, 0);
+                return;
             }
+#pragma unroll
+            for (int i = 0; i < VPT; ++i) {
+                if (VCH % (kWaves * kWave) == 0 || tid + i * kWaves * kWave < VCH) {
+                    rv0[i] = __builtin_amdgcn_raw_buffer_load_b128(rq, ovb[i], so, 0);
+                    rv1[i] = __builtin_amdgcn_raw_buffer_load_b128(rq, ovb[i] + D3 * 2, so, 0);
+                }
+            }
+            return;
+        }
+#pragma unroll
+        for (int i = 0; i < KLW; ++i) {
+            int tok = kv0 + krow[i];
+            tok = tok < L ? tok : L - 1;
+            __builtin_amdgcn_global_load_lds(Kg + static_cast<size_t>(seq0 + tok) * D3 + kch[i] * 8,
+                                             (lds_t*)(k_s + i * KRL * DH), 16, 0, 0);
+        }
+        if constexpr (VDIRECT) {
+            uint16_t* v_d = sVt + b * VBUF + wsc * 16 * DH;
+#pragma unroll
+            for (int i = 0; i < KLW; ++i) {
+                int tok = kv0 + krow[i];
+                tok = tok < L ? tok : L - 1;
+                __builtin_amdgcn_global_load_lds(Vg + static_cast<size_t>(seq0 + tok) * D3 + vch[i] * 8,
+                                                 (lds_t*)(v_d + i * KRL * DH), 16, 0, 0);
+            }
+            return;
         }
 #pragma unroll
         for (int i = 0; i < VPT; ++i) {
@@ -154,16 +235,8 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
         }
     };
     auto sstore = [&](int b) {
-        uint16_t* k_s = sK + b * (kBKV * DH);
-        uint16_t* v_s = sVt + b * (DH * kVtStride);
-#pragma unroll
-        for (int i = 0; i < KPT; ++i) {
-            const int c = tid + i * kWaves * kWave;
-            if (KCH % (kWaves * kWave) == 0 || c < KCH) {
-                const int row = c / CPR, ch = c % CPR;
-                *reinterpret_cast<u32x4*>(&k_s[row * DH + ((ch ^ kswz<DH>(row)) * 8)]) = rk[i];
-            }
-        }
+        if constexpr (VDIRECT) return;
+        uint16_t* v_s = sVt + b * VBUF;
 #pragma unroll
         for (int i = 0; i < VPT; ++i) {
             const int u = tid + i * kWaves * kWave;
@@ -184,17 +257,20 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     };
 
     const int ntiles = (L + kBKV - 1) / kBKV;
-    gload(0);
+    gload(0, 0);
     for (int t = 0; t < ntiles; ++t) {
         const int kv0 = t * kBKV;
         const int b = t & 1;
-        // Buffer b was last read in tile t-2; the barrier of tile t-1 ordered those reads
-        // before these writes.
+        // V of tile t into buffer b (last read in tile t-2, ordered by the barrier of tile t-1);
+        // K of tile t was loaded into it directly. This wave's loads are all complete here, and
+        // the barrier makes every wave's part of the tile visible.
         sstore(b);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt and lgkmcnt unconstrained: this wave's direct loads have landed
         __syncthreads();
-        if (t + 1 < ntiles) gload(kv0 + kBKV);  // in flight while this tile is multiplied
+        // Buffer b^1 (tile t-1) is free: every wave has passed this barrier, so none still reads it.
+        if (t + 1 < ntiles) gload(kv0 + kBKV, b ^ 1);  // in flight while this tile is multiplied
         const uint16_t* k_s = sK + b * (kBKV * DH);
-        const uint16_t* v_s = sVt + b * (DH * kVtStride);
+        const uint16_t* v_s = sVt + b * VBUF;
 
         if (qw >= q_end) continue;  // this wave's queries are all past the end (uniform per wave)
 
@@ -280,7 +356,20 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
                 // keys {kc*32 + 4g .. +3, kc*32 + 16 + 4g .. +3}: 16 contiguous bytes in V^T
-                const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&v_s[d * kVtStride + kc * 32 + 8 * g]);
+                bf16x8 vf;
+                if constexpr (VDIRECT) {
+                    // Lane 4r + q of a 16-lane group points at key 32 kc + 4 g + r (then + 16),
+                    // d-columns dt * 16 + 4 q .. +3; the transposed read hands lane i of the group
+                    // those 4 keys of column dt * 16 + i: the 8 keys of the P^T operand's k-slots.
+                    const int j16 = lane & 15, r = j16 >> 2, q = j16 & 3;
+                    const int row = kc * 32 + 4 * g + r;
+                    const lds_cu16* p0 = (lds_cu16*)(v_s) + row * DH + (4 * (dt ^ vswz_m(row)) + q) * 4;
+                    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0));
+                    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 16 * DH));
+                    vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                } else {
+                    vf = *reinterpret_cast<const bf16x8*>(&v_s[d * kVtStride + kc * 32 + 8 * g]);
+                }
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     o[dt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[kc][j], o[dt][j], 0, 0, 0);
@@ -307,6 +396,7 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
             *reinterpret_cast<u32x2*>(orow + dt * 16 + 4 * g) = pk;
         }
     }
+#endif
 }
 
 }  // namespace
@@ -319,10 +409,10 @@ hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total,
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
     if (dh == 64)
         ELIS_TRY(launch_kernel(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2, cls_only ? 1 : 0));
+                           out, scale_log2, cls_only ? 1 : 0, total));
     else if (dh == 32)
         ELIS_TRY(launch_kernel(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2, cls_only ? 1 : 0));
+                           out, scale_log2, cls_only ? 1 : 0, total));
     else
         return hipErrorInvalidValue;
     return hipSuccess;
