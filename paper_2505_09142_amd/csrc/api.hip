@@ -113,8 +113,8 @@ bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) % kAlign) =
 
 // ------------------------------------------------------------------ workspace layout
 struct PredictLayout {
-    size_t status, start, len, tile_off, x32, xb, qkv, attn, ha, hb, sa, sb, ffn, pool_partial, pool_z, head_hid,
-        total;
+    size_t status, start, len, tile_off, work, x32, xb, qkv, attn, ha, hb, sa, sb, ffn, pool_partial, pool_z,
+        head_hid, total;
     int nchunk;
 };
 
@@ -131,6 +131,7 @@ PredictLayout predict_layout(const elis_config& c, int T, int n, int max_seqlen)
     p.start = take(sizeof(int32_t) * n);
     p.len = take(sizeof(int32_t) * n);
     p.tile_off = take(sizeof(int32_t) * (n + 1));
+    if (c.n_layers > 0) p.work = take(4 * sizeof(int32_t) * static_cast<size_t>(attn_work_capacity(n, T)));
     p.x32 = take(4 * t * d);
     if (c.n_layers > 0) {
         p.xb = take(2 * t * d);
@@ -196,8 +197,9 @@ PoolHeadLayout pool_head_layout(const elis_config& c, int n, int max_seqlen) {
     return p;
 }
 
-size_t attention_ws(int n) {
-    return align_up(sizeof(uint32_t)) + 2 * align_up(sizeof(int32_t) * n) + align_up(sizeof(int32_t) * (n + 1));
+size_t attention_ws(int n, int total) {
+    return align_up(sizeof(uint32_t)) + 2 * align_up(sizeof(int32_t) * n) + align_up(sizeof(int32_t) * (n + 1)) +
+           align_up(4 * sizeof(int32_t) * static_cast<size_t>(attn_work_capacity(n, total)));
 }
 
 template <class T>
@@ -287,7 +289,7 @@ int elis_predict_remaining(const elis_weights* w, const int32_t* token_ids, cons
     const int T = total_tokens, n = n_seqs, d = c.d_model, F = c.d_ff, L = c.n_layers;
     uint32_t* status = at<uint32_t>(workspace, p.status);
     const SeqTable tab{at<int32_t>(workspace, p.start), at<int32_t>(workspace, p.len),
-                       at<int32_t>(workspace, p.tile_off)};
+                       at<int32_t>(workspace, p.tile_off), L ? at<int32_t>(workspace, p.work) : nullptr};
     float* x32 = at<float>(workspace, p.x32);
     float* final32 = out_hidden ? out_hidden : x32;
     uint16_t* xb = L ? at<uint16_t>(workspace, p.xb) : nullptr;
@@ -633,7 +635,7 @@ int elis_linear_with_plan(const uint16_t* x, const uint16_t* w, const float* bia
 
 size_t elis_attention_workspace_bytes(int32_t n_seqs, int32_t total_tokens) {
     if (n_seqs <= 0 || total_tokens < n_seqs) return 0;
-    return attention_ws(n_seqs);
+    return attention_ws(n_seqs, total_tokens);
 }
 
 int elis_attention(const uint16_t* qkv, const int32_t* cu_seqlens, int32_t n_seqs, int32_t total_tokens,
@@ -644,7 +646,7 @@ int elis_attention(const uint16_t* qkv, const int32_t* cu_seqlens, int32_t n_seq
     if (!aligned(workspace)) return ELIS_EINVAL;
     if (d_head != 32 && d_head != 64) return ELIS_EUNSUPPORTED;
     if (total_tokens < n_seqs || max_seqlen < 1) return ELIS_ESHAPE;
-    if (ws_bytes < attention_ws(n_seqs)) return ELIS_EWORKSPACE;
+    if (ws_bytes < attention_ws(n_seqs, total_tokens)) return ELIS_EWORKSPACE;
     hipStream_t st = static_cast<hipStream_t>(stream);
     size_t o = 0;
     uint32_t* status = at<uint32_t>(workspace, o);
@@ -655,6 +657,8 @@ int elis_attention(const uint16_t* qkv, const int32_t* cu_seqlens, int32_t n_seq
     tab.len = at<int32_t>(workspace, o);
     o += align_up(sizeof(int32_t) * n_seqs);
     tab.tile_off = at<int32_t>(workspace, o);
+    o += align_up(sizeof(int32_t) * (n_seqs + 1));
+    tab.work = at<int32_t>(workspace, o);
     hipError_t e = timed(ELIS_K_SEQMAP,
                          [&] { return launch_seqmap(cu_seqlens, n_seqs, total_tokens, max_seqlen, tab, status, st); });
     if (e != hipSuccess) return status_of(e);

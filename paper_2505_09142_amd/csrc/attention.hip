@@ -86,7 +86,8 @@ template <int DH>
 __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t* __restrict__ qkv,
                                                                   const int32_t* __restrict__ seq_start,
                                                                   const int32_t* __restrict__ seq_len,
-                                                                  const int32_t* __restrict__ tile_off, int n,
+                                                                  const int32_t* __restrict__ tile_off,
+                                                                  const int32_t* __restrict__ work, int n,
                                                                   int H, uint16_t* __restrict__ out,
                                                                   float scale_log2, int cls_only, int total) {
 // The body is device code only: the host pass has no buffer-resource type, and a kernel whose
@@ -102,14 +103,27 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     constexpr int VBUF = VDIRECT ? kBKV * DH : DH * kVtStride;
     __shared__ __attribute__((aligned(16))) uint16_t sVt[2 * VBUF];
 
-    const int tile = blockIdx.x, h = blockIdx.y;
-    // cls_only: one work-group per (sequence, head) computing the first 32 queries (wave 0,
-    // exactly as in the full launch, so the CLS query sees the same arithmetic) and writing the
-    // CLS row alone, to row s of a one-row-per-sequence output.
-    if (cls_only ? tile >= n : tile >= tile_off[n]) return;  // uniform over the work-group
-    const int s = cls_only ? tile : find_segment(tile_off, n, tile);
-    const int seq0 = seq_start[s], L = seq_len[s];
-    const int q0 = cls_only ? 0 : (tile - tile_off[s]) * kBQ;
+    // Work-group w runs head w % H of work item w / H: the heads of one query tile are
+    // adjacent, and the items come longest sequence first (the work list's order).
+    // cls_only: item s is sequence s, one work-group per (sequence, head) computing the first
+    // 32 queries (wave 0, exactly as in the full launch, so the CLS query sees the same
+    // arithmetic) and writing the CLS row alone, to row s of a one-row-per-sequence output.
+    const int item = blockIdx.x / H, h = blockIdx.x - item * H;
+    int s, seq0, L, q0;
+    if (cls_only) {
+        s = item;
+        seq0 = seq_start[s];
+        L = seq_len[s];
+        q0 = 0;
+    } else {
+        // The grid holds the list's capacity, so the entry is in bounds even past the count.
+        const int4 e = *reinterpret_cast<const int4*>(work + 4 * static_cast<size_t>(item));
+        if (item >= tile_off[n]) return;  // uniform over the work-group
+        seq0 = e.x;
+        L = e.y;
+        q0 = e.z;
+        s = e.w;
+    }
     const int q_end = cls_only ? (L < kQPerWave ? L : kQPerWave) : L;  // queries computed
 
     const int D = H * DH, D3 = 3 * D;
@@ -403,16 +417,19 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 
 hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh, uint16_t* out,
                             hipStream_t st, bool cls_only) {
-    // Upper bound of sum_s ceil(len_s / kBQ); surplus work-groups exit at once.
-    const int tiles = cls_only ? n : (total + kBQ - 1) / kBQ + n;
-    const dim3 grid(tiles, heads), block(kWaves * kWave);
+    // The work list's capacity (an upper bound of sum_s ceil(len_s / kBQ)); surplus
+    // work-groups exit at once.
+    if (!cls_only && !tab.work) return hipErrorInvalidValue;
+    const int items = cls_only ? n : attn_work_capacity(n, total);
+    if (static_cast<long long>(items) * heads > 0x7fffffffLL) return hipErrorInvalidValue;
+    const dim3 grid(items * heads), block(kWaves * kWave);
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
     if (dh == 64)
-        ELIS_TRY(launch_kernel(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2, cls_only ? 1 : 0, total));
+        ELIS_TRY(launch_kernel(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off,
+                           tab.work, n, heads, out, scale_log2, cls_only ? 1 : 0, total));
     else if (dh == 32)
-        ELIS_TRY(launch_kernel(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off, n, heads,
-                           out, scale_log2, cls_only ? 1 : 0, total));
+        ELIS_TRY(launch_kernel(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off,
+                           tab.work, n, heads, out, scale_log2, cls_only ? 1 : 0, total));
     else
         return hipErrorInvalidValue;
     return hipSuccess;

@@ -69,14 +69,21 @@ constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Sequence table written by the seq-map kernel: sanitised start/length of
-// every sequence plus the exclusive prefix of attention query tiles.
+// every sequence, the exclusive prefix of attention query tiles and, when work
+// is not null, the attention work list: one entry {start, length, first query,
+// sequence} per query tile, longest sequences first.
 struct SeqTable {
     int32_t* start;     // [n]
     int32_t* len;       // [n]
     int32_t* tile_off;  // [n + 1]
+    int32_t* work = nullptr;  // [4 * attn_work_capacity(n, total)]
 };
 
 // Rows per attention work-group (query tile) used to build the tile table.
 constexpr int kAttnRowsPerBlock = 128;
+
+// Entries of the attention work list: sum_s ceil(len_s / 128) <= total / 128 + n for
+// lengths that partition the batch; entries past it (malformed lengths) are dropped.
+inline int attn_work_capacity(int n, int total) { return (total + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock + n; }
 
 }  // namespace elis
