@@ -82,14 +82,13 @@ __device__ __forceinline__ float quad_max(float v) {
     return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));  // {l & 31, l | 32}
 }
 
-template <int DH>
+template <int DH, bool CLS>
 __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t* __restrict__ qkv,
                                                                   const int32_t* __restrict__ seq_start,
                                                                   const int32_t* __restrict__ seq_len,
-                                                                  const int32_t* __restrict__ tile_off,
-                                                                  const int32_t* __restrict__ work, int n,
-                                                                  int H, uint16_t* __restrict__ out,
-                                                                  float scale_log2, int cls_only, int total) {
+                                                                  const int32_t* __restrict__ work, int H,
+                                                                  uint16_t* __restrict__ out, float scale_log2,
+                                                                  int total) {
 // The body is device code only: the host pass has no buffer-resource type, and a kernel whose
 // body it cannot form would lose its host-side launch stub.
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -104,27 +103,27 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     __shared__ __attribute__((aligned(16))) uint16_t sVt[2 * VBUF];
 
     // Work-group w runs head w % H of work item w / H: the heads of one query tile are
-    // adjacent, and the items come longest sequence first (the work list's order).
-    // cls_only: item s is sequence s, one work-group per (sequence, head) computing the first
-    // 32 queries (wave 0, exactly as in the full launch, so the CLS query sees the same
-    // arithmetic) and writing the CLS row alone, to row s of a one-row-per-sequence output.
+    // adjacent, and the items come longest sequence first (the work list's order; slots
+    // past the list's end hold length 0). CLS: item s is sequence s, one work-group per
+    // (sequence, head) computing the first 32 queries (wave 0, exactly as in the full launch,
+    // so the CLS query sees the same arithmetic) and writing the CLS row alone, to row s of a
+    // one-row-per-sequence output.
     const int item = blockIdx.x / H, h = blockIdx.x - item * H;
     int s, seq0, L, q0;
-    if (cls_only) {
+    if constexpr (CLS) {
         s = item;
         seq0 = seq_start[s];
         L = seq_len[s];
         q0 = 0;
     } else {
-        // The grid holds the list's capacity, so the entry is in bounds even past the count.
         const int4 e = *reinterpret_cast<const int4*>(work + 4 * static_cast<size_t>(item));
-        if (item >= tile_off[n]) return;  // uniform over the work-group
         seq0 = e.x;
         L = e.y;
         q0 = e.z;
         s = e.w;
+        if ((L <= 0) | (q0 < 0)) return;  // uniform; q0 >= 0 always, tested so the entry is loaded whole here
     }
-    const int q_end = cls_only ? (L < kQPerWave ? L : kQPerWave) : L;  // queries computed
+    const int q_end = CLS ? (L < kQPerWave ? L : kQPerWave) : L;  // queries computed
 
     const int D = H * DH, D3 = 3 * D;
     const uint16_t* Qg = qkv + h * DH;
@@ -400,8 +399,8 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     for (int j = 0; j < 2; ++j) {
         const float inv = 1.0f / lsum[j][0];
         const int qi = qw + j * 16 + r16;
-        if (cls_only ? qi != 0 : qi >= L) continue;
-        uint16_t* orow = out + static_cast<size_t>(cls_only ? s : seq0 + qi) * D + h * DH;
+        if (CLS ? qi != 0 : qi >= L) continue;
+        uint16_t* orow = out + static_cast<size_t>(CLS ? s : seq0 + qi) * D + h * DH;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
             u32x2 pk;
@@ -418,18 +417,20 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
 hipError_t launch_attention(const uint16_t* qkv, SeqTable tab, int n, int total, int heads, int dh, uint16_t* out,
                             hipStream_t st, bool cls_only) {
     // The work list's capacity (an upper bound of sum_s ceil(len_s / kBQ)); surplus
-    // work-groups exit at once.
+    // work-groups find length 0 and exit at once.
     if (!cls_only && !tab.work) return hipErrorInvalidValue;
     const int items = cls_only ? n : attn_work_capacity(n, total);
     if (static_cast<long long>(items) * heads > 0x7fffffffLL) return hipErrorInvalidValue;
     const dim3 grid(items * heads), block(kWaves * kWave);
     const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
+    auto go = [&](auto kernel) {
+        return launch_kernel(kernel, grid, block, 0, st, qkv, tab.start, tab.len, tab.work, heads, out, scale_log2,
+                             total);
+    };
     if (dh == 64)
-        ELIS_TRY(launch_kernel(attention_kernel<64>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off,
-                           tab.work, n, heads, out, scale_log2, cls_only ? 1 : 0, total));
+        ELIS_TRY(cls_only ? go(attention_kernel<64, true>) : go(attention_kernel<64, false>));
     else if (dh == 32)
-        ELIS_TRY(launch_kernel(attention_kernel<32>, grid, block, 0, st, qkv, tab.start, tab.len, tab.tile_off,
-                           tab.work, n, heads, out, scale_log2, cls_only ? 1 : 0, total));
+        ELIS_TRY(cls_only ? go(attention_kernel<32, true>) : go(attention_kernel<32, false>));
     else
         return hipErrorInvalidValue;
     return hipSuccess;

@@ -9,7 +9,8 @@
 // longest sequence first (a counting sort on the number of 64-key tiles, lengths
 // above 64 such tiles sharing the top bucket; batch order within a bucket), and
 // each entry carries the tile's sequence start, length and first query, so a
-// work-group reads its whole assignment with one load.
+// work-group reads its whole assignment with one load; slots past the list's end
+// hold length 0, and their work-groups exit.
 #include "kernels.h"
 
 namespace elis {
@@ -99,6 +100,8 @@ __global__ __launch_bounds__(kThreads) void seqmap_kernel(const int32_t* __restr
         *status = flags_s;
     }
     if (!work) return;  // uniform
+    for (int idx = carry_s + tid; idx < work_cap; idx += kThreads)  // unused slots: length 0
+        *reinterpret_cast<int4*>(work + 4 * static_cast<size_t>(idx)) = make_int4(0, 0, 0, 0);
     if (wid == 0) {  // bucket bases, longest bucket first: lane l scans bucket kBuckets - 1 - l
         const int c = hist[kBuckets - 1 - lane];
         bucket_base[kBuckets - 1 - lane] = wave_incl_scan(c, lane) - c;

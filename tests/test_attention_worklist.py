@@ -3,10 +3,12 @@
 1. The seq-map kernel's attention work list (seqmap.hip): a counting sort of the
    query tiles on each sequence's number of 64-key tiles (capped at 64), longest
    first, batch order inside a bucket, built per 1024-thread chunk from in-wave
-   ranks, per-wave bucket totals and per-bucket carries. Checked: the entries
-   written are a bijection onto [0, min(count, capacity)), every write lies below
-   the capacity the workspace holds, the order is longest first and stable, and
-   each entry names the right (start, length, first query).
+   ranks, per-wave bucket totals and per-bucket carries; the slots between the
+   count and the capacity get length 0. Checked: the entries written are a
+   bijection onto [0, min(count, capacity)), every write lies below the capacity
+   the workspace holds (the attention grid's size, so every work-group reads a
+   written slot), the order is longest first and stable, and each entry names the
+   right (sequence, query tile).
 2. The d_head-64 V tile (attention.hip): direct-to-LDS loads place row R's
    logical 16-byte chunk c at physical chunk c ^ (2 * ((R >> 1) & 3)); the PV
    operand is read with ds_read_b64_tr_b16, whose result for lane i of a 16-lane
@@ -73,6 +75,9 @@ def build_work_list(lens, cap):
                         work[idx] = (s, q)
         for b in range(KB):
             carry[b] += int(wave_b[:, b].sum())
+    for idx in range(sum(tiles), cap):  # slots past the list's end: length 0, the work-group exits
+        assert idx not in work
+        work[idx] = None
     return work, sum(tiles)
 
 
@@ -80,7 +85,8 @@ def check_list(lens, total):
     cap = capacity(len(lens), total)
     work, count = build_work_list(lens, cap)
     m = min(count, cap)
-    assert sorted(work) == list(range(m))
+    assert sorted(work) == list(range(cap))  # every slot of the grid reads a written entry
+    assert all(work[i] is None for i in range(m, cap)) and all(work[i] is not None for i in range(m))
     keys = [(-bucket(lens[work[i][0]]), work[i][0], work[i][1]) for i in range(m)]
     assert keys == sorted(keys), "not longest first, batch order within a bucket"
     if count <= cap:  # every query tile of every sequence listed once
@@ -112,7 +118,7 @@ def test_work_list_over_capacity_is_clipped():
     lens = [9000, 7, 1]
     cap = 10
     work, count = build_work_list(lens, cap)
-    assert count > cap and sorted(work) == list(range(cap))
+    assert count > cap and sorted(work) == list(range(cap)) and None not in work.values()
 
 
 def test_v_tile_direct_load_and_transposed_read():
