@@ -90,7 +90,7 @@ def check_list(lens, total):
     keys = [(-bucket(lens[work[i][0]]), work[i][0], work[i][1]) for i in range(m)]
     assert keys == sorted(keys), "not longest first, batch order within a bucket"
     if count <= cap:  # every query tile of every sequence listed once
-        assert sorted(work.values()) == sorted((s, q) for s, L in enumerate(lens) for q in range((L + RPB - 1) // RPB))
+        assert sorted(work[i] for i in range(m)) == sorted((s, q) for s, L in enumerate(lens) for q in range((L + RPB - 1) // RPB))
     return count, cap
 
 
@@ -141,7 +141,6 @@ def test_v_tile_direct_load_and_transposed_read():
     assert lds.min() >= 0
     for kc in range(2):
         for dt in range(DH // 16):
-            banks = {}
             addr = np.zeros((KW, 2), dtype=np.int64)
             for lane in range(KW):
                 g, j16 = lane // 16, lane % 16
