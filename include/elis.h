@@ -14,9 +14,9 @@
  * Conventions for every call below:
  *  - All data pointers are DEVICE pointers owned by the caller, unless a
  *    comment says "host". The library allocates no device memory, never frees
- *    caller memory and keeps no state between calls (except the opt-in
- *    timing facility at the end of this file, and the fixed per-device
- *    scratch of elis_isrtf_select_noalloc).
+ *    caller memory and keeps no state between calls (except the opt-in,
+ *    per-thread timing facility at the end of this file, and the fixed
+ *    per-device scratch of elis_isrtf_select_noalloc).
  *  - Every call validates its scalar arguments on the host, then only
  *    enqueues kernels on `stream` (a hipStream_t; NULL = the default stream)
  *    and returns. Nothing synchronises except elis_read_status and
@@ -393,8 +393,9 @@ int elis_pool_head(const elis_weights *w, const float *hidden, const int32_t *cu
  * last reset is timed; the others run untimed. elis_timing_read synchronises
  * the pending events and returns, per class, the number of timed launches and
  * their summed kernel time (a launch that enqueues several kernels counts
- * once, with the sum of its kernels' times). Process-global state; not
- * thread-safe; meant for benchmarks.
+ * once, with the sum of its kernels' times). The state is per host thread:
+ * each call acts on the calling thread's own records, and launches made by
+ * other threads are not timed. Meant for benchmarks.
  */
 #define ELIS_K_SEQMAP    0
 #define ELIS_K_EMBED_LN  1

@@ -20,21 +20,26 @@ struct TimedLaunch {
     bool first;
     hipEvent_t a, b;
 };
-uint32_t g_timing_mask = 0;
-std::vector<TimedLaunch> g_pending;
-std::vector<hipEvent_t> g_free_events;
-double g_ms[ELIS_K_COUNT];
-int32_t g_count[ELIS_K_COUNT];
-uint32_t g_stride = 1;              // time one class launch in every g_stride
-uint64_t g_seen[ELIS_K_COUNT];       // class launches enqueued since the last reset
-int g_timed_cls = -1;  // class being enqueued under timing, else -1
-bool g_timed_first = false;
-bool g_timing_failed = false;
+// The state belongs to the calling host thread (thread_local): enabling, timed launches,
+// reset and read act on that thread's records only, so threads never share it.
+struct TimingState {
+    uint32_t mask = 0;
+    std::vector<TimedLaunch> pending;
+    std::vector<hipEvent_t> free_events;
+    double ms[ELIS_K_COUNT] = {};
+    int32_t count[ELIS_K_COUNT] = {};
+    uint32_t stride = 1;             // time one class launch in every `stride`
+    uint64_t seen[ELIS_K_COUNT] = {};  // class launches enqueued since the last reset
+    int timed_cls = -1;              // class being enqueued under timing, else -1
+    bool timed_first = false;
+    bool failed = false;
+};
+thread_local TimingState g_t;
 
 hipEvent_t take_event() {
-    if (!g_free_events.empty()) {
-        hipEvent_t e = g_free_events.back();
-        g_free_events.pop_back();
+    if (!g_t.free_events.empty()) {
+        hipEvent_t e = g_t.free_events.back();
+        g_t.free_events.pop_back();
         return e;
     }
     hipEvent_t e = nullptr;
@@ -46,23 +51,23 @@ hipEvent_t take_event() {
 // carries its own start/stop events (launch_timing_events below).
 template <class F>
 hipError_t timed(int cls, F&& launch) {
-    if (!(g_timing_mask & (1u << cls))) return launch();
-    if (g_seen[cls]++ % g_stride != 0) return launch();
-    const size_t mark = g_pending.size();
-    g_timed_cls = cls;
-    g_timed_first = true;
-    g_timing_failed = false;
+    if (!(g_t.mask & (1u << cls))) return launch();
+    if (g_t.seen[cls]++ % g_t.stride != 0) return launch();
+    const size_t mark = g_t.pending.size();
+    g_t.timed_cls = cls;
+    g_t.timed_first = true;
+    g_t.failed = false;
     const hipError_t e = launch();
-    g_timed_cls = -1;
+    g_t.timed_cls = -1;
     if (e != hipSuccess) {  // drop the records of a class launch that did not complete
-        for (size_t i = mark; i < g_pending.size(); ++i) {
-            g_free_events.push_back(g_pending[i].a);
-            g_free_events.push_back(g_pending[i].b);
+        for (size_t i = mark; i < g_t.pending.size(); ++i) {
+            g_t.free_events.push_back(g_t.pending[i].a);
+            g_t.free_events.push_back(g_t.pending[i].b);
         }
-        g_pending.resize(mark);
+        g_t.pending.resize(mark);
         return e;
     }
-    return g_timing_failed ? hipErrorOutOfMemory : hipSuccess;
+    return g_t.failed ? hipErrorOutOfMemory : hipSuccess;
 }
 
 int status_of(hipError_t e) {
@@ -232,16 +237,16 @@ int run_linear(const GemmPlan& p, const uint16_t* x, const uint16_t* w, const fl
 
 bool elis::launch_timing_events(hipEvent_t* start, hipEvent_t* stop) {
     *start = *stop = nullptr;
-    if (g_timed_cls < 0) return false;
+    if (g_t.timed_cls < 0) return false;
     hipEvent_t a = take_event(), b = take_event();
     if (!a || !b) {
-        if (a) g_free_events.push_back(a);
-        if (b) g_free_events.push_back(b);
-        g_timing_failed = true;
+        if (a) g_t.free_events.push_back(a);
+        if (b) g_t.free_events.push_back(b);
+        g_t.failed = true;
         return false;
     }
-    g_pending.push_back({g_timed_cls, g_timed_first, a, b});
-    g_timed_first = false;
+    g_t.pending.push_back({g_t.timed_cls, g_t.timed_first, a, b});
+    g_t.timed_first = false;
     *start = a;
     *stop = b;
     return true;
@@ -692,45 +697,45 @@ int elis_linear_plan(int32_t m, int32_t n, int32_t k, int32_t epilogue, int32_t*
 }
 
 int elis_timing_enable(uint32_t class_mask) {
-    g_timing_mask = class_mask & ((1u << ELIS_K_COUNT) - 1);
+    g_t.mask = class_mask & ((1u << ELIS_K_COUNT) - 1);
     return ELIS_OK;
 }
 
 int elis_timing_stride(int32_t every) {
     if (every < 1) return ELIS_EINVAL;
-    g_stride = static_cast<uint32_t>(every);
+    g_t.stride = static_cast<uint32_t>(every);
     return ELIS_OK;
 }
 
 int elis_timing_reset(void) {
-    for (auto& t : g_pending) {
+    for (auto& t : g_t.pending) {
         (void)hipEventSynchronize(t.b);
-        g_free_events.push_back(t.a);
-        g_free_events.push_back(t.b);
+        g_t.free_events.push_back(t.a);
+        g_t.free_events.push_back(t.b);
     }
-    g_pending.clear();
+    g_t.pending.clear();
     for (int i = 0; i < ELIS_K_COUNT; ++i) {
-        g_ms[i] = 0.0;
-        g_count[i] = 0;
-        g_seen[i] = 0;
+        g_t.ms[i] = 0.0;
+        g_t.count[i] = 0;
+        g_t.seen[i] = 0;
     }
     return ELIS_OK;
 }
 
 int elis_timing_read(int32_t kernel_class, int32_t* launches, double* total_ms) {
     if (kernel_class < 0 || kernel_class >= ELIS_K_COUNT || !launches || !total_ms) return ELIS_EINVAL;
-    for (auto& t : g_pending) {
+    for (auto& t : g_t.pending) {
         if (hipEventSynchronize(t.b) != hipSuccess) return ELIS_EHIP;
         float ms = 0.f;
         if (hipEventElapsedTime(&ms, t.a, t.b) != hipSuccess) return ELIS_EHIP;
-        g_ms[t.cls] += ms;
-        g_count[t.cls] += t.first ? 1 : 0;
-        g_free_events.push_back(t.a);
-        g_free_events.push_back(t.b);
+        g_t.ms[t.cls] += ms;
+        g_t.count[t.cls] += t.first ? 1 : 0;
+        g_t.free_events.push_back(t.a);
+        g_t.free_events.push_back(t.b);
     }
-    g_pending.clear();
-    *launches = g_count[kernel_class];
-    *total_ms = g_ms[kernel_class];
+    g_t.pending.clear();
+    *launches = g_t.count[kernel_class];
+    *total_ms = g_t.ms[kernel_class];
     return ELIS_OK;
 }
 
