@@ -1,4 +1,4 @@
-// Device building blocks shared by the matrix-core kernels (gemm.hip, gemm_ln.hip): the MFMA
+// Device building blocks of the matrix-core product kernels (gemm.hip): the MFMA
 // block types, the XCD-aware work-group remap, direct-to-LDS loads and wait-count helpers.
 #pragma once
 
