@@ -35,10 +35,12 @@ CFLAGS = [
 # tile; keeping them in VGPRs (not AGPRs) avoids a register-file round trip per rescale. Its
 # arithmetic never forms a NaN from finite inputs (masked scores are -inf, the running maximum
 # starts at -inf and is finite after the first tile), so maxima need no NaN canonicalisation.
-# Its kernel arguments are preloaded into SGPRs at wave launch (the work-group's first scalar
-# load is then its work-list entry; 52.5 -> 51.9 us per BERT-base layer).
+# Its kernel arguments, and the product kernels', are preloaded into SGPRs at wave launch (the
+# attention work-group's first scalar load is then its work-list entry: 52.5 -> 51.9 us per
+# BERT-base layer; the products gain ~0.5 us per launch).
 EXTRA = {
     "attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans", "-mllvm", "-amdgpu-kernarg-preload-count=16"],
+    "gemm.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=16"],
 }
 
 
