@@ -82,25 +82,26 @@ __device__ __forceinline__ float quad_max(float v) {
     return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));  // {l & 31, l | 32}
 }
 
+// Four waves per SIMD (at most 128 VGPRs): with 32 KB of LDS per work-group, four work-groups
+// share a CU and cover one another's tile loads and barriers.
 template <int DH, bool CLS>
-__global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t* __restrict__ qkv,
-                                                                  const int32_t* __restrict__ seq_start,
-                                                                  const int32_t* __restrict__ seq_len,
-                                                                  const int32_t* __restrict__ work, int H,
-                                                                  uint16_t* __restrict__ out, float scale_log2,
-                                                                  int total) {
+__global__ __launch_bounds__(kWaves* kWave) __attribute__((amdgpu_waves_per_eu(4))) void attention_kernel(
+    const uint16_t* __restrict__ qkv, const int32_t* __restrict__ seq_start, const int32_t* __restrict__ seq_len,
+    const int32_t* __restrict__ work, int H, uint16_t* __restrict__ out, float scale_log2, int total) {
 // The body is device code only: the host pass has no buffer-resource type, and a kernel whose
 // body it cannot form would lose its host-side launch stub.
 #if defined(__HIP_DEVICE_COMPILE__)
     constexpr int CPR = DH / 8;   // 16-byte chunks per head row
     constexpr int KS = DH / 32;   // MFMA k-steps over d_head
     constexpr int DT = DH / 16;   // 16-wide d blocks of the output
-    __shared__ __attribute__((aligned(16))) uint16_t sK[2 * kBKV * DH];
+    // Two buffers, one array each: the compiler tracks direct-to-LDS loads per LDS variable, so
+    // the loads into one buffer do not make it wait before reading the other.
+    __shared__ __attribute__((aligned(16))) uint16_t sK0[kBKV * DH], sK1[kBKV * DH];
     // d_head 64: V tiles row-major (8-byte units XOR-swizzled by row pair, see vswz), read back
     // transposed by ds_read_b64_tr_b16; d_head 32: V^T rows staged through registers (vt_pos).
     constexpr bool VDIRECT = DH == 64;
     constexpr int VBUF = VDIRECT ? kBKV * DH : DH * kVtStride;
-    __shared__ __attribute__((aligned(16))) uint16_t sVt[2 * VBUF];
+    __shared__ __attribute__((aligned(16))) uint16_t sV0[VBUF], sV1[VBUF];
 
     // Work-group w runs head w % H of work item w / H: the heads of one query tile are
     // adjacent, and the items come longest sequence first (the work list's order; slots
@@ -193,15 +194,15 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
         ovb[i] = static_cast<uint32_t>(((seq0 + 2 * (u % (kBKV / 2))) * D3 + 2 * D + h * DH + (u / (kBKV / 2)) * 8) * 2);
     }
     typedef __attribute__((address_space(3))) void lds_t;
-    auto gload = [&](int kv0, int b) {
-        uint16_t* k_s = sK + b * (kBKV * DH) + wsc * 16 * DH;
+    auto gload = [&](int kv0, uint16_t* kd, uint16_t* vd) {
+        uint16_t* k_s = kd + wsc * 16 * DH;
         if (offs32 && kv0 + kBKV <= L) {
             const int so = kv0 * D3 * 2;
 #pragma unroll
             for (int i = 0; i < KLW; ++i)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_t*)(k_s + i * KRL * DH), 16, okb[i], so, 0, 0);
             if constexpr (VDIRECT) {
-                uint16_t* v_d = sVt + b * VBUF + wsc * 16 * DH;
+                uint16_t* v_d = vd + wsc * 16 * DH;
 #pragma unroll
                 for (int i = 0; i < KLW; ++i)
                     __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_t*)(v_d + i * KRL * DH), 16, ovd[i], so, 0, 0);
@@ -224,7 +225,7 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                                              (lds_t*)(k_s + i * KRL * DH), 16, 0, 0);
         }
         if constexpr (VDIRECT) {
-            uint16_t* v_d = sVt + b * VBUF + wsc * 16 * DH;
+            uint16_t* v_d = vd + wsc * 16 * DH;
 #pragma unroll
             for (int i = 0; i < KLW; ++i) {
                 int tok = kv0 + krow[i];
@@ -247,9 +248,8 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
             }
         }
     };
-    auto sstore = [&](int b) {
+    auto sstore = [&](uint16_t* v_s) {
         if constexpr (VDIRECT) return;
-        uint16_t* v_s = sVt + b * VBUF;
 #pragma unroll
         for (int i = 0; i < VPT; ++i) {
             const int u = tid + i * kWaves * kWave;
@@ -270,22 +270,31 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
     };
 
     const int ntiles = (L + kBKV - 1) / kBKV;
-    gload(0, 0);
-    for (int t = 0; t < ntiles; ++t) {
+    // Transposed V reads (d_head 64): lane 4r + q of a 16-lane group, d block dt, addresses key
+    // row 4 g + r (+ 32 kc, + 16) at d columns 16 dt + 4 q, swizzled as the direct loads placed
+    // it. The lane part is formed once, so each read's address is a short chain from its array.
+    int vo[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+        const int j16 = lane & 15, row = 4 * g + (j16 >> 2);
+        vo[dt] = row * DH + (4 * (dt ^ vswz_m(row)) + (j16 & 3)) * 4;
+    }
+    gload(0, sK0, sV0);
+    // Tile t: K and V in buffer t % 2 (k_s, vb), tile t + 1 loaded into the other (kn, vn);
+    // unrolled twice so each buffer is a fixed array.
+    auto tile = [&](int t, const uint16_t* k_s, uint16_t* vb, uint16_t* kn, uint16_t* vn) {
         const int kv0 = t * kBKV;
-        const int b = t & 1;
-        // V of tile t into buffer b (last read in tile t-2, ordered by the barrier of tile t-1);
+        // V of tile t into buffer t % 2 (last read in tile t-2, ordered by the barrier of tile t-1);
         // K of tile t was loaded into it directly. This wave's loads are all complete here, and
         // the barrier makes every wave's part of the tile visible.
-        sstore(b);
+        sstore(vb);
         __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt and lgkmcnt unconstrained: this wave's direct loads have landed
         __syncthreads();
-        // Buffer b^1 (tile t-1) is free: every wave has passed this barrier, so none still reads it.
-        if (t + 1 < ntiles) gload(kv0 + kBKV, b ^ 1);  // in flight while this tile is multiplied
-        const uint16_t* k_s = sK + b * (kBKV * DH);
-        const uint16_t* v_s = sVt + b * VBUF;
+        // The other buffer (tile t-1) is free: every wave has passed this barrier, so none still reads it.
+        if (t + 1 < ntiles) gload(kv0 + kBKV, kn, vn);  // in flight while this tile is multiplied
+        const uint16_t* v_s = vb;
 
-        if (qw >= q_end) continue;  // this wave's queries are all past the end (uniform per wave)
+        if (qw >= q_end) return;  // this wave's queries are all past the end (uniform per wave)
 
         // S^T = K Q^T: 4 key blocks x 2 query blocks (raw scores, unscaled).
         f32x4 sc[4][2];
@@ -374,9 +383,7 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
                     // Lane 4r + q of a 16-lane group points at key 32 kc + 4 g + r (then + 16),
                     // d-columns dt * 16 + 4 q .. +3; the transposed read hands lane i of the group
                     // those 4 keys of column dt * 16 + i: the 8 keys of the P^T operand's k-slots.
-                    const int j16 = lane & 15, r = j16 >> 2, q = j16 & 3;
-                    const int row = kc * 32 + 4 * g + r;
-                    const lds_cu16* p0 = (lds_cu16*)(v_s) + row * DH + (4 * (dt ^ vswz_m(row)) + q) * 4;
+                    const lds_cu16* p0 = (lds_cu16*)(v_s) + vo[dt] + kc * 32 * DH;
                     const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0));
                     const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 16 * DH));
                     vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
@@ -392,6 +399,10 @@ __global__ __launch_bounds__(kWaves* kWave) void attention_kernel(const uint16_t
         for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
             for (int j = 0; j < 2; ++j) lsum[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[kc][j], lsum[j], 0, 0, 0);
+    };
+    for (int t = 0; t < ntiles; t += 2) {
+        tile(t, sK0, sV0, sK1, sV1);
+        if (t + 1 < ntiles) tile(t + 1, sK1, sV1, sK0, sV0);
     }
 
     // Normalise and store: lane holds O[query j*16 + r16][d = dt*16 + 4g .. +3].

@@ -147,6 +147,10 @@ def test_v_tile_direct_load_and_transposed_read():
                 r, q = j16 >> 2, j16 & 3
                 row = kc * 32 + 4 * g + r
                 p0 = row * DH + (4 * (dt ^ ((row >> 1) & 3)) + q) * 4
+                # The kernel forms the lane part once (key row 4 g + r) and adds 32 kc rows:
+                # the swizzle reads bits 1-2 of the row, which 32 kc leaves alone.
+                r0 = 4 * g + r
+                assert p0 == r0 * DH + (4 * (dt ^ ((r0 >> 1) & 3)) + q) * 4 + kc * 32 * DH
                 for h, p in enumerate((p0, p0 + 16 * DH)):
                     assert 0 <= p and p + 4 <= vbuf
                     addr[lane, h] = p
