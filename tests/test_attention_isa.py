@@ -6,8 +6,8 @@ explicit vmcnt wait) only before the next barrier. The compiler tracks such dire
 loads by LDS variable: when both buffers were one array it could not tell the buffer being
 loaded from the one being read, and put a vmcnt(0) wait before the first LDS read of every
 tile, so each tile waited out the next one's loads. This test compiles attention.hip for gfx950
-with the library's flags and checks, in the all-queries kernel, that between a direct-to-LDS
-load and the next barrier no LDS read is preceded by a vmcnt wait.
+with the library's flags and checks, in the all-queries kernel and the CLS-only one, that between
+a direct-to-LDS load and the next barrier no LDS read is preceded by a vmcnt wait.
 """
 import os
 import re
@@ -18,14 +18,17 @@ import pytest
 
 from paper_2505_09142_amd import build as B
 
-KERNEL = "_ZN4elis12_GLOBAL__N_116attention_kernelILi64ELb0EEEvPKtPKiS5_S5_iPtfi"
+KERNELS = {  # all queries; the CLS-only tail of the last layer
+    "all": "_ZN4elis12_GLOBAL__N_116attention_kernelILi64ELb0EEEvPKtPKiS5_S5_iPtfi",
+    "cls": "_ZN4elis12_GLOBAL__N_116attention_kernelILi64ELb1EEEvPKtPKiS5_S5_iPtfi",
+}
 DMA = re.compile(r"^\s*(buffer_load_dword\S*\s.*\blds\b|global_load_lds_dword\S*)")
 WAIT = re.compile(r"^\s*s_waitcnt\s.*vmcnt\(")
 READ = re.compile(r"^\s*ds_read")
 BARRIER = re.compile(r"^\s*s_barrier\b")
 
 
-def kernel_asm(tmp_path):
+def kernel_asm(tmp_path, kernel):
     if not os.path.exists(B.HIPCC) and shutil.which("hipcc") is None:
         pytest.skip("hipcc not available")
     src = os.path.join(B.CSRC, "attention.hip")
@@ -34,7 +37,7 @@ def kernel_asm(tmp_path):
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = out.read_text().split("\n")
-    start = next(i for i, l in enumerate(lines) if l.startswith(KERNEL + ":"))
+    start = next(i for i, l in enumerate(lines) if l.startswith(kernel + ":"))
     end = next(i for i in range(start, len(lines)) if lines[i].strip().startswith("s_endpgm"))
     return lines[start:end]
 
@@ -79,8 +82,9 @@ def blocks(body):
     return order, cfg
 
 
-def test_no_wait_on_tile_loads_before_lds_reads(tmp_path):
-    body = kernel_asm(tmp_path)
+@pytest.mark.parametrize("which", sorted(KERNELS))
+def test_no_wait_on_tile_loads_before_lds_reads(tmp_path, which):
+    body = kernel_asm(tmp_path, KERNELS[which])
     assert any(DMA.match(l) for l in body), "no direct-to-LDS loads found"
     order, cfg = blocks(body)
     # Forward dataflow over the control-flow graph. State bits: A = a direct-to-LDS load was
